@@ -1,0 +1,32 @@
+"""Build the CPU oracle (plain C, gcc) into oracle/libpic_oracle.so.
+
+Test infrastructure: the oracle is what the decoder's results are checked
+against.  ``-ffp-contract=off`` keeps every multiply and add of the fp64 and
+fp32 models rounded exactly as written in the source.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "pic_oracle.c")
+LIB = os.path.join(HERE, "libpic_oracle.so")
+
+
+def build(verbose: bool = False, src: str = SRC, out: str = LIB) -> str:
+    """Compile ``src`` (default: the oracle) into the shared library ``out``."""
+    tmp = out + f".tmp{os.getpid()}"
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src, "-lm"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
+if __name__ == "__main__":
+    build(verbose=True)
+    sys.exit(0)

@@ -1,0 +1,65 @@
+"""Planted mistakes in the oracle, on the CPU: each plausible slip in
+pic_oracle.c (a dropped term, a wrong sign or index, a transposed operand, a
+misplaced clamp) is compiled into a throw-away copy, and at least one pin in
+tests/pins.py must reject that copy.  This shows the pins constrain every part
+of the oracle, not just that the oracle agrees with itself."""
+import os
+import re
+import tempfile
+
+import pytest
+
+import oracle
+from oracle import build as obuild
+from tests import pins
+
+# (name, exact source fragment of the fp64 path, replacement)
+MUTANTS = [
+    ("drop_bias", "acc += (double)bias[bo + j];", ""),
+    ("transpose_weights", "long idx = wo + (long)j * fin + i;\n                        double wv",
+     "long idx = wo + (long)i * fout + j;\n                        double wv"),
+    ("relu_on_last_layer", "g[j] = (l < nl - 1 && acc < 0.0) ? 0.0 : acc;",
+     "g[j] = (acc < 0.0) ? 0.0 : acc;"),
+    ("no_relu", "g[j] = (l < nl - 1 && acc < 0.0) ? 0.0 : acc;", "g[j] = acc;"),
+    ("no_half_pixel", "double sy = ((double)y + 0.5) / f - 0.5;", "double sy = (double)y / f;"),
+    ("swap_axes", "double ly = sy - y0, lx = sx - x0;", "double ly = sx - x0, lx = sy - y0;"),
+    ("wrap_edge", "floor(sx);\n    int y1 = y0 + 1 < hk ? y0 + 1 : hk - 1;",
+     "floor(sx);\n    int y1 = y0 + 1 < hk ? y0 + 1 : 0;"),
+    ("no_low_clamp", "    if (sx < 0.0) sx = 0.0;\n    int y0", "    int y0"),
+    ("flipped_lerp", "double top = (1.0 - lx) * a + lx * b;", "double top = lx * a + (1.0 - lx) * b;"),
+    ("levels_reversed", "h[k] = upsample_f64(grid, hk[k], wk[k], k, y, x);",
+     "h[L - 1 - k] = upsample_f64(grid, hk[k], wk[k], k, y, x);"),
+    ("floor_level_dims", "return (int)((n + f - 1) / f);", "return (int)(n / f);"),
+    ("u8_truncates", "((uint8_t *)out)[o] = (uint8_t)floor(255.0 * cl + 0.5);",
+     "((uint8_t *)out)[o] = (uint8_t)floor(255.0 * cl);"),
+    ("no_upper_clamp", "double cl = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);",
+     "double cl = v < 0.0 ? 0.0 : v;"),
+    ("wrong_output_plane", "size_t o = (((size_t)b * 3 + c) * H + y) * (size_t)W + x;\n                double v",
+     "size_t o = (((size_t)b * 3 + (2 - c)) * H + y) * (size_t)W + x;\n                double v"),
+    ("f32_model_no_bias", "float acc = bias[bo + j];", "float acc = 0.0f;"),
+    ("f32_model_transposed", "long idx = wo + (long)j * fin + i;\n                        float wv",
+     "long idx = wo + (long)i * fout + j;\n                        float wv"),
+    ("f32_model_u8_truncates", "(uint8_t)floorf(fmaf(cl, 255.0f, 0.5f))", "(uint8_t)floorf(cl * 255.0f)"),
+]
+
+
+def _caught(orc):
+    for check in pins.ALL_CHECKS:
+        try:
+            check(orc)
+        except (AssertionError, ValueError):
+            return check.__name__
+    return None
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, old, new, tmp_path):
+    src = open(obuild.SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique in pic_oracle.c"
+    mutated = src.replace(old, new)
+    csrc = tmp_path / "mutant.c"
+    csrc.write_text(mutated)
+    lib = str(tmp_path / f"libmutant_{name}.so")
+    obuild.build(src=str(csrc), out=lib)
+    orc = oracle.Oracle(lib)
+    assert _caught(orc) is not None, f"no pin rejects the {name} mutant"
