@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Benchmark of the PIC synthesis decoder on one MI355X.
+
+A step is one pic_decode_run call: the whole synthesis path (upsample of every
+latent level + the per-pixel MLP + epilogue) over one batch of synthetic,
+device-resident inputs.  W untimed warm-up steps, then exactly K timed steps
+bracketed by torch.cuda.synchronize(); the kernel's own duration is measured
+live with HIP events recorded on the stream the kernel is launched on.
+
+Prints ONE JSON line: decoded Mpixel/s (value), FPS, ms per step, the
+roofline of the dominant kernel and the CPU oracle's throughput on a bounded
+sample of the same workload (rank 0, N = 1 only).
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload kodak768]
+                  [--variant auto|valu|mfma_f32|mfma_bf16] [--out-dtype f32|u8]
+                  [--no-cpu-baseline] [--copy-calib]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decoded Mpixel/s (and FPS at 768x512) on 1 MI355X; % of roofline"
+# MI355X published peaks.
+PEAK_FP32_TFLOPS = 157.3        # fp32 vector (packed) and fp32 matrix
+PEAK_BF16_TFLOPS = 2500.0       # dense bf16 matrix
+PEAK_HBM_GBS = 8000.0
+
+
+def flops_per_pixel(widths):
+    """Algorithmic work per pixel: 2 * sum(in * out) for the MLP (bias folded
+    into the accumulator start) + 8 * (L - 1) for the bilinear upsample of the
+    L - 1 coarser levels (3 lerps of a multiply and an add, plus weights)."""
+    L = widths[0]
+    return 2 * sum(widths[i] * widths[i + 1] for i in range(len(widths) - 1)) + 8 * (L - 1)
+
+
+def bytes_per_call(wl, out_dtype):
+    """Compulsory HBM bytes: every latent read once, every output written once,
+    every image's parameters read once."""
+    from paper_2609_09020_amd import synth
+    lat = sum(h * w for h, w in (synth.level_shape(wl.height, wl.width, k) for k in range(wl.levels)))
+    nw, nb = synth.param_counts(wl.widths)
+    wbytes = 2 if wl.weight_dtype == "bf16" else 4
+    out_b = 1 if out_dtype == "u8" else 4
+    return wl.batch * (4 * lat + 3 * out_b * wl.height * wl.width + wbytes * nw + 4 * nb)
+
+
+def load_traffic(kernel, workload, out_dtype):
+    """Measured HBM traffic per launch from the committed counter summary, if
+    it was taken on the current kernel source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{out_dtype}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2609_09020_amd", "csrc", kv.get("source", ""))
+    if not os.path.exists(src):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if sha != kv.get("source_sha256_16"):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, inp, target_s=12.0):
+    """The fp64 oracle, as it stands, on the host cores: whole images of the
+    workload, repeated until about target_s seconds of CPU work."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    orc = oracle.default()
+    n_img = 0
+    t0 = time.perf_counter()
+    while True:
+        b = n_img % inp.batch
+        orc.decode_inputs(inp, out="clamped", batch_slice=slice(b, b + 1), nthreads=threads)
+        n_img += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    px = n_img * wl.height * wl.width
+    return {"value": round(px / dt / 1e6, 3), "unit": "Mpixel/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_img} whole {wl.width}x{wl.height} image decode(s) of this workload by the "
+                      f"fp64 C oracle (OpenMP over rows), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--workload", default="kodak768")
+    ap.add_argument("--variant", default="auto")
+    ap.add_argument("--out-dtype", default="f32", choices=["f32", "u8"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also run a plain device copy of known size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on exactly one GPU (the decoder has no multi-GPU "
+              "path); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_09020_amd import synth
+    from paper_2609_09020_amd import decoder as D
+
+    wl = synth.WORKLOADS[args.workload]
+    inp = synth.workload_inputs(wl)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
+    if inp.weights_bf16 is not None:
+        w = torch.from_numpy(inp.weights_bf16.view(np.int16)).to(dev)
+    else:
+        w = torch.from_numpy(inp.weights).to(dev)
+    b = torch.from_numpy(inp.biases).to(dev)
+    dec = D.Decoder(wl.height, wl.width, wl.widths, weight_dtype=wl.weight_dtype,
+                    out_dtype=args.out_dtype, max_batch=wl.batch, variant=args.variant)
+    out = dec.alloc_out(wl.batch, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # Pre-marshalled raw call: the loop measures the library, not Python checks.
+    import ctypes
+    lib = D.load_library()
+    lat_arr = (ctypes.c_void_p * len(lat))(*[t.data_ptr() for t in lat])
+    run_args = (ctypes.c_void_p(dec.handle), ctypes.c_int32(wl.batch), lat_arr,
+                ctypes.c_void_p(w.data_ptr()), ctypes.c_int64(dec.nw),
+                ctypes.c_void_p(b.data_ptr()), ctypes.c_int64(dec.nb),
+                ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+    run = lib.pic_decode_run
+
+    for _ in range(args.warmup):
+        st = run(*run_args)
+        if st != D.PIC_OK:
+            raise D.PicError(st, "pic_decode_run")
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record(stream)
+        run(*run_args)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = [s.elapsed_time(e) for s, e in ev]
+    kern_avg_ms = float(np.mean(kern_ms))
+    kern_med_ms = float(np.median(kern_ms))
+
+    # Latency mode (synchronise, decode, synchronise) over single calls.
+    lat_n = min(200, max(20, K // 10))
+    tl = 0.0
+    for _ in range(lat_n):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        run(*run_args)
+        torch.cuda.synchronize()
+        tl += time.perf_counter() - t1
+    latency_ms = 1e3 * tl / lat_n
+
+    if args.copy_calib:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)   # 256 MiB
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    info = dec.info()
+    px = wl.batch * wl.height * wl.width
+    ms_per_step = 1e3 * elapsed / K
+    mpx_s = px * K / elapsed / 1e6
+    fpp = flops_per_pixel(wl.widths)
+    flop = px * fpp
+    kernel = info["kernel_name"]
+    if info["variant"] == "mfma_bf16":
+        bound, peak, unit = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s"
+    elif info["variant"] == "mfma_f32":
+        bound, peak, unit = "mfma", PEAK_FP32_TFLOPS, "TFLOP/s"
+    else:
+        bound, peak, unit = "alu", PEAK_FP32_TFLOPS, "TFLOP/s"
+    achieved = flop / (kern_avg_ms * 1e-3) / 1e12
+    traffic = load_traffic(kernel, args.workload, args.out_dtype)
+    res = {
+        "metric": METRIC, "value": round(mpx_s, 2), "unit": "Mpixel/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if wl.weight_dtype == "bf16" else "f32", "data": "synthetic",
+        "fps": round(wl.batch * K / elapsed, 1),
+        "latency_ms": round(latency_ms, 4),
+        "kernel_avg_ms": round(kern_avg_ms, 5), "kernel_median_ms": round(kern_med_ms, 5),
+        "config": {"workload": f"{wl.name}: {wl.note}", "height": wl.height, "width": wl.width,
+                   "levels": wl.levels, "widths": list(wl.widths), "batch": wl.batch,
+                   "weights": wl.weight_dtype, "out_dtype": args.out_dtype,
+                   "variant": info["variant"], "kernel": kernel, "parallelism": "single GPU"},
+        "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                     "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "flop_per_launch": flop, "flop_per_pixel": fpp,
+                     "compulsory_bytes_per_launch": bytes_per_call(wl, args.out_dtype),
+                     "hbm_frac_at_compulsory_bytes": round(
+                         bytes_per_call(wl, args.out_dtype) / (kern_avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, inp)
+    dec.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

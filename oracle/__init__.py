@@ -21,11 +21,12 @@ OUT_RAW, OUT_CLAMPED, OUT_U8 = 0, 1, 2
 def _bind(path):
     lib = ctypes.CDLL(path)
     # (H, W, L, nl, widths, batch, latents, weights, is_bf16, w_stride,
-    #  biases, b_stride, out_kind, out, nthreads)
+    #  biases, b_stride, out_kind, out, nthreads, y_begin, y_end)
     argt = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_int, ctypes.c_long,
                                  ctypes.c_void_p, ctypes.c_long,
-                                 ctypes.c_int, ctypes.c_void_p, ctypes.c_int]
+                                 ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                 ctypes.c_int, ctypes.c_int]
     for name in ("pic_oracle_decode_f64", "pic_oracle_decode_f32"):
         fn = getattr(lib, name)
         fn.restype = ctypes.c_int
@@ -76,7 +77,7 @@ class Oracle:
     def decode(self, latents: Sequence[np.ndarray], weights: np.ndarray, biases: np.ndarray,
                widths: Sequence[int], height: int, width: int, out: str = "clamped",
                precision: str = "f64", weights_bf16: np.ndarray = None,
-               shared: bool = False, nthreads: int = 0) -> np.ndarray:
+               shared: bool = False, nthreads: int = 0, rows: tuple = None) -> np.ndarray:
         """Decode a batch on the CPU.
 
         latents: L float32 arrays [batch][H_k][W_k]; weights float32 [batch][nw]
@@ -84,7 +85,8 @@ class Oracle:
         ``weights_bf16`` (uint16 bit patterns, same shape as weights) replaces
         the float32 weights when given.  ``out`` is "raw", "clamped" or "u8";
         ``precision`` is "f64" (the definition) or "f32" (binary32 model).
-        Returns [batch][3][H][W] float64 / float32 / uint8.
+        ``rows`` = (y_begin, y_end) computes only those output rows.
+        Returns [batch][3][rows][W] float64 / float32 / uint8.
         """
         widths = [int(w) for w in widths]
         L, nl = len(latents), len(widths) - 1
@@ -113,26 +115,27 @@ class Oracle:
             dt = np.uint8
         else:
             dt = np.float64 if precision == "f64" else np.float32
-        res = np.empty((batch, 3, height, width), dtype=dt)
+        y0, y1 = (0, height) if rows is None else (int(rows[0]), int(rows[1]))
+        res = np.empty((batch, 3, max(0, y1 - y0), width), dtype=dt)
         wid = (ctypes.c_int * len(widths))(*widths)
         fn = {"f64": self._lib.pic_oracle_decode_f64,
               "f32": self._lib.pic_oracle_decode_f32}[precision]
         rc = fn(height, width, L, nl, wid, batch, ptrs, w.ctypes.data, is_bf16, w_stride,
-                b.ctypes.data, b_stride, kind, res.ctypes.data, nthreads)
+                b.ctypes.data, b_stride, kind, res.ctypes.data, nthreads, y0, y1)
         if rc:
             raise ValueError("oracle rejected the arguments")
         del keep
         return res
 
     def decode_inputs(self, inp, out: str = "clamped", precision: str = "f64",
-                      nthreads: int = 0, batch_slice: slice = None) -> np.ndarray:
-        """decode() on a synth.Inputs bundle (optionally a slice of its images)."""
+                      nthreads: int = 0, batch_slice: slice = None, rows: tuple = None) -> np.ndarray:
+        """decode() on a synth.Inputs bundle (optionally some images / rows)."""
         sl = batch_slice or slice(None)
         lat = [a[sl] for a in inp.latents]
         wb = inp.weights_bf16[sl] if inp.weights_bf16 is not None else None
         return self.decode(lat, inp.weights[sl], inp.biases[sl], inp.widths, inp.height,
                            inp.width, out=out, precision=precision, weights_bf16=wb,
-                           nthreads=nthreads)
+                           nthreads=nthreads, rows=rows)
 
 
 _default = None

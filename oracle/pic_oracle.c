@@ -126,31 +126,36 @@ static double upsample_f64(const float *grid, int hk, int wk, int k, int y, int 
  *                 elements (0: all images share one set)
  *   biases      : float32, per image, layer l's widths[l+1] values concatenated;
  *                 image b starts at b * b_stride
- *   out         : [batch][3][H][W] planar, double for raw / clamped output,
- *                 uint8 for 8-bit output
+ *   out         : [batch][3][y_end - y_begin][W] planar, double for raw /
+ *                 clamped output, uint8 for 8-bit output
  *   nthreads    : OpenMP threads (<= 0: the runtime's default)
+ *   y_begin, y_end : the output rows computed (0 and H for the whole image);
+ *                 a row's values do not depend on which other rows are computed
  * Returns 0, or 1 on invalid arguments (nothing written).
  */
 int pic_oracle_decode_f64(int H, int W, int L, int nl, const int *widths, int batch,
                           const float *const *latents,
                           const void *weights, int weights_are_bf16, long w_stride,
                           const float *biases, long b_stride,
-                          int out_kind, void *out, int nthreads)
+                          int out_kind, void *out, int nthreads, int y_begin, int y_end)
 {
     if (check_args(H, W, L, nl, widths, batch, latents, weights, biases, out, out_kind))
         return OR_E_INVALID;
+    if (y_begin < 0 || y_end > H || y_begin >= y_end)
+        return OR_E_INVALID;
+    const int R = y_end - y_begin;
     int hk[OR_MAX_LEVELS], wk[OR_MAX_LEVELS];
     for (int k = 0; k < L; ++k) {
         hk[k] = pic_oracle_level_dim(H, k);
         wk[k] = pic_oracle_level_dim(W, k);
     }
-    long rows = (long)batch * H;
+    long rows = (long)batch * R;
 #ifdef _OPENMP
     int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
 #endif
     for (long r = 0; r < rows; ++r) {
-        int b = (int)(r / H), y = (int)(r % H);
+        int b = (int)(r / R), y = y_begin + (int)(r % R);
         const float *fw = (const float *)weights + (weights_are_bf16 ? 0 : b * w_stride);
         const uint16_t *hw = (const uint16_t *)weights + (weights_are_bf16 ? b * w_stride : 0);
         const float *bias = biases + b * b_stride;
@@ -178,7 +183,7 @@ int pic_oracle_decode_f64(int H, int W, int L, int nl, const int *widths, int ba
                 bo += fout;
             }
             for (int c = 0; c < 3; ++c) {
-                size_t o = (((size_t)b * 3 + c) * H + y) * (size_t)W + x;
+                size_t o = (((size_t)b * 3 + c) * R + (y - y_begin)) * (size_t)W + x;
                 double v = h[c];
                 double cl = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
                 if (out_kind == OR_OUT_RAW)
@@ -227,22 +232,25 @@ int pic_oracle_decode_f32(int H, int W, int L, int nl, const int *widths, int ba
                           const float *const *latents,
                           const void *weights, int weights_are_bf16, long w_stride,
                           const float *biases, long b_stride,
-                          int out_kind, void *out, int nthreads)
+                          int out_kind, void *out, int nthreads, int y_begin, int y_end)
 {
     if (check_args(H, W, L, nl, widths, batch, latents, weights, biases, out, out_kind))
         return OR_E_INVALID;
+    if (y_begin < 0 || y_end > H || y_begin >= y_end)
+        return OR_E_INVALID;
+    const int R = y_end - y_begin;
     int hk[OR_MAX_LEVELS], wk[OR_MAX_LEVELS];
     for (int k = 0; k < L; ++k) {
         hk[k] = pic_oracle_level_dim(H, k);
         wk[k] = pic_oracle_level_dim(W, k);
     }
-    long rows = (long)batch * H;
+    long rows = (long)batch * R;
 #ifdef _OPENMP
     int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
 #endif
     for (long r = 0; r < rows; ++r) {
-        int b = (int)(r / H), y = (int)(r % H);
+        int b = (int)(r / R), y = y_begin + (int)(r % R);
         const float *fw = (const float *)weights + (weights_are_bf16 ? 0 : b * w_stride);
         const uint16_t *hw = (const uint16_t *)weights + (weights_are_bf16 ? b * w_stride : 0);
         const float *bias = biases + b * b_stride;
@@ -269,7 +277,7 @@ int pic_oracle_decode_f32(int H, int W, int L, int nl, const int *widths, int ba
                 bo += fout;
             }
             for (int c = 0; c < 3; ++c) {
-                size_t o = (((size_t)b * 3 + c) * H + y) * (size_t)W + x;
+                size_t o = (((size_t)b * 3 + c) * R + (y - y_begin)) * (size_t)W + x;
                 float v = h[c];
                 float cl = fminf(fmaxf(v, 0.0f), 1.0f);
                 if (out_kind == OR_OUT_RAW)

@@ -5,3 +5,6 @@ level of a latent pyramid to full resolution and evaluate a small ReLU MLP per
 pixel to RGB.  The work runs in hand-written HIP kernels behind a C ABI
 (``include/pic_decode.h``); this package is the thin Python binding over it.
 """
+
+from .decoder import (Decoder, PicError, load_library, make_desc, pic_decode_create,  # noqa: F401
+                      pic_decode_destroy, pic_decode_query, pic_decode_run, pic_status_string)

@@ -1,0 +1,236 @@
+// C ABI of the PIC synthesis decoder: argument validation, variant choice and
+// launch on the caller's stream.  The kernels live in k_*.hip.
+#include <hip/hip_runtime.h>
+
+#include <new>
+#include <stdio.h>
+#include <string.h>
+
+#include "pic_decode.h"
+#include "pic_internal.h"
+
+struct pic_decoder {
+    pic_decode_desc desc;
+    int32_t variant;            // resolved pic_variant (never AUTO)
+    int32_t device;
+    int32_t num_cus;
+    int64_t weights_per_image;
+    int64_t biases_per_image;
+    int32_t px_per_step;
+    char kernel_name[64];
+};
+
+namespace {
+
+int32_t level_dim(int32_t n, int k) { return (int32_t)(((int64_t)n + (1LL << k) - 1) >> k); }
+
+pic_status validate_desc(const pic_decode_desc *d)
+{
+    if (!d || d->struct_size != sizeof(pic_decode_desc))
+        return PIC_E_INVALID;
+    if (d->height < 1 || d->width < 1 || (int64_t)d->height * d->width >= (1LL << 31))
+        return PIC_E_INVALID;
+    if (d->num_levels < 1 || d->num_levels > PIC_MAX_LEVELS)
+        return PIC_E_INVALID;
+    if (d->num_layers < 1 || d->num_layers > PIC_MAX_LAYERS)
+        return PIC_E_INVALID;
+    if (d->widths[0] != d->num_levels || d->widths[d->num_layers] != 3)
+        return PIC_E_INVALID;
+    for (int l = 1; l < d->num_layers; ++l)
+        if (d->widths[l] < 1 || d->widths[l] > PIC_MAX_WIDTH)
+            return PIC_E_INVALID;
+    if (d->weight_dtype != PIC_F32 && d->weight_dtype != PIC_BF16)
+        return PIC_E_INVALID;
+    if (d->out_dtype != PIC_F32 && d->out_dtype != PIC_U8)
+        return PIC_E_INVALID;
+    if (d->flags & ~(uint32_t)PIC_FLAG_NO_CLAMP)
+        return PIC_E_INVALID;
+    if ((d->flags & PIC_FLAG_NO_CLAMP) && d->out_dtype != PIC_F32)
+        return PIC_E_INVALID;
+    if (d->max_batch < 1 || d->max_batch > PIC_MAX_BATCH)
+        return PIC_E_INVALID;
+    if (d->variant < PIC_VARIANT_AUTO || d->variant > PIC_VARIANT_MFMA_BF16)
+        return PIC_E_INVALID;
+    return PIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pic_status_string(pic_status s)
+{
+    switch (s) {
+    case PIC_OK: return "ok";
+    case PIC_E_INVALID: return "invalid argument";
+    case PIC_E_UNSUPPORTED: return "unsupported configuration";
+    case PIC_E_NODEVICE: return "no gfx950 HIP device";
+    case PIC_E_HIP: return "HIP runtime error";
+    case PIC_E_NOMEM: return "out of host memory";
+    }
+    return "unknown status";
+}
+
+pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
+{
+    if (!out)
+        return PIC_E_INVALID;
+    *out = nullptr;
+    pic_status st = validate_desc(desc);
+    if (st != PIC_OK)
+        return st;
+
+    const int L = desc->num_levels, nl = desc->num_layers;
+    int32_t variant = desc->variant;
+    if (variant == PIC_VARIANT_AUTO) {
+        // Matrix cores where the family covers the shape, else the reference family.
+        if (desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths))
+            variant = PIC_VARIANT_MFMA_BF16;
+        else if (desc->weight_dtype == PIC_F32 && pic::mfma_f32_supports(L, nl, desc->widths))
+            variant = PIC_VARIANT_MFMA_F32;
+        else
+            variant = PIC_VARIANT_VALU;
+    }
+    bool ok = false;
+    switch (variant) {
+    case PIC_VARIANT_VALU: ok = pic::valu_supports(L, nl, desc->widths); break;
+    case PIC_VARIANT_MFMA_F32: ok = pic::mfma_f32_supports(L, nl, desc->widths); break;
+    case PIC_VARIANT_MFMA_BF16:
+        ok = desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths);
+        break;
+    }
+    if (!ok)
+        return PIC_E_UNSUPPORTED;
+
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+        (void)hipGetLastError();
+        return PIC_E_NODEVICE;
+    }
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return PIC_E_NODEVICE;
+    }
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return PIC_E_NODEVICE;
+
+    pic_decoder *d = new (std::nothrow) pic_decoder;
+    if (!d)
+        return PIC_E_NOMEM;
+    memset(d, 0, sizeof *d);
+    d->desc = *desc;
+    d->variant = variant;
+    d->device = dev;
+    d->num_cus = prop.multiProcessorCount;
+    for (int l = 0; l < nl; ++l) {
+        d->weights_per_image += (int64_t)desc->widths[l] * desc->widths[l + 1];
+        d->biases_per_image += desc->widths[l + 1];
+    }
+    *out = d;
+    return PIC_OK;
+}
+
+pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *latents,
+                          const void *weights, int64_t weights_img_stride,
+                          const float *biases, int64_t biases_img_stride,
+                          void *out, void *stream)
+{
+    if (!dec)
+        return PIC_E_INVALID;
+    const pic_decode_desc &d = dec->desc;
+    if (batch < 0 || batch > d.max_batch)
+        return PIC_E_INVALID;
+    if (weights_img_stride < 0 || biases_img_stride < 0)
+        return PIC_E_INVALID;
+    if (batch == 0)
+        return PIC_OK;
+    if (!latents || !weights || !biases || !out)
+        return PIC_E_INVALID;
+    const size_t walign = d.weight_dtype == PIC_BF16 ? 2 : 4;
+    if (((uintptr_t)weights % walign) || ((uintptr_t)biases % 4))
+        return PIC_E_INVALID;
+    if (d.out_dtype == PIC_F32 && ((uintptr_t)out % 4))
+        return PIC_E_INVALID;
+    // Per-image parameter blocks must not overlap unless shared.
+    if (weights_img_stride != 0 && weights_img_stride < dec->weights_per_image)
+        return PIC_E_INVALID;
+    if (biases_img_stride != 0 && biases_img_stride < dec->biases_per_image)
+        return PIC_E_INVALID;
+
+    pic::DecodeParams p;
+    memset(&p, 0, sizeof p);
+    for (int k = 0; k < d.num_levels; ++k) {
+        if (!latents[k] || ((uintptr_t)latents[k] % 4))
+            return PIC_E_INVALID;
+        p.lat[k] = latents[k];
+        p.hk[k] = level_dim(d.height, k);
+        p.wk[k] = level_dim(d.width, k);
+    }
+    p.H = d.height;
+    p.W = d.width;
+    p.L = d.num_levels;
+    p.nl = d.num_layers;
+    int32_t wo = 0, bo = 0;
+    for (int l = 0; l <= d.num_layers; ++l)
+        p.widths[l] = d.widths[l];
+    for (int l = 0; l < d.num_layers; ++l) {
+        p.woff[l] = wo;
+        p.boff[l] = bo;
+        wo += d.widths[l] * d.widths[l + 1];
+        bo += d.widths[l + 1];
+    }
+    p.weights = weights;
+    p.w_stride = weights_img_stride;
+    p.biases = biases;
+    p.b_stride = biases_img_stride;
+    p.out = out;
+    p.out_kind = d.out_dtype == PIC_U8 ? pic::OUT_U8
+               : (d.flags & PIC_FLAG_NO_CLAMP) ? pic::OUT_RAW_F32 : pic::OUT_CLAMPED_F32;
+    p.weights_bf16 = d.weight_dtype == PIC_BF16;
+    p.batch = batch;
+    p.groups_per_image = (int32_t)(((int64_t)d.height * d.width + 15) / 16);
+
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != dec->device) {
+        (void)hipGetLastError();
+        return PIC_E_INVALID;   // the handle belongs to another device
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const char *name = nullptr;
+    int pxs = 0;
+    hipError_t e = hipErrorInvalidValue;
+    switch (dec->variant) {
+    case PIC_VARIANT_VALU: e = pic::launch_valu(p, s, &name, &pxs); break;
+    case PIC_VARIANT_MFMA_F32: e = pic::launch_mfma_f32(p, s, &name, &pxs, dec->num_cus); break;
+    case PIC_VARIANT_MFMA_BF16: e = pic::launch_mfma_bf16(p, s, &name, &pxs, dec->num_cus); break;
+    }
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return PIC_E_HIP;
+    }
+    if (name) {
+        strncpy(dec->kernel_name, name, sizeof dec->kernel_name - 1);
+        dec->px_per_step = pxs;
+    }
+    return PIC_OK;
+}
+
+pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info)
+{
+    if (!dec || !info || info->struct_size != sizeof(pic_decode_info))
+        return PIC_E_INVALID;
+    info->variant = dec->variant;
+    info->weights_per_image = dec->weights_per_image;
+    info->biases_per_image = dec->biases_per_image;
+    info->device = dec->device;
+    info->pixels_per_wave_step = dec->px_per_step;
+    memset(info->kernel_name, 0, sizeof info->kernel_name);
+    strncpy(info->kernel_name, dec->kernel_name, sizeof info->kernel_name - 1);
+    return PIC_OK;
+}
+
+void pic_decode_destroy(pic_decoder *dec) { delete dec; }
+
+}  // extern "C"

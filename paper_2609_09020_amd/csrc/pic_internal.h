@@ -1,0 +1,49 @@
+// Internal interface between the C ABI (pic_decode.hip) and the kernel
+// translation units.  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pic_decode.h"
+
+namespace pic {
+
+// Output encodings of the epilogue.
+enum OutKind : int32_t { OUT_RAW_F32 = 0, OUT_CLAMPED_F32 = 1, OUT_U8 = 2 };
+
+// Everything a decode kernel needs, passed by value as the kernel argument.
+struct DecodeParams {
+    const float *lat[PIC_MAX_LEVELS];   // level k base pointer, [batch][hk][wk]
+    int32_t hk[PIC_MAX_LEVELS];         // ceil(H / 2^k)
+    int32_t wk[PIC_MAX_LEVELS];         // ceil(W / 2^k)
+    int32_t H, W, L, nl;                // image size, levels, linear layers
+    int32_t widths[PIC_MAX_LAYERS + 1];
+    int32_t woff[PIC_MAX_LAYERS];       // element offset of layer l's matrix
+    int32_t boff[PIC_MAX_LAYERS];       // element offset of layer l's bias
+    const void *weights;                // fp32 or bf16 elements
+    int64_t w_stride;                   // elements between images (0: shared)
+    const float *biases;
+    int64_t b_stride;
+    void *out;                          // [batch][3][H][W]
+    int32_t out_kind;                   // OutKind
+    int32_t weights_bf16;               // 1: weights are bf16 bit patterns
+    int32_t batch;
+    int32_t groups_per_image;           // 16-pixel groups per image (MFMA kernels)
+};
+
+// Kernel launchers: return hipSuccess or the launch error.  Each checks that
+// the shape it is asked for is one it was instantiated for (returns
+// hipErrorInvalidValue otherwise, nothing launched).
+hipError_t launch_valu(const DecodeParams &p, hipStream_t s, const char **name, int *px_per_step);
+hipError_t launch_mfma_f32(const DecodeParams &p, hipStream_t s, const char **name, int *px_per_step,
+                           int num_cus);
+hipError_t launch_mfma_bf16(const DecodeParams &p, hipStream_t s, const char **name, int *px_per_step,
+                            int num_cus);
+
+// Shape support queries used at create time (no device needed).
+bool valu_supports(int L, int nl, const int32_t *widths);
+bool mfma_f32_supports(int L, int nl, const int32_t *widths);
+bool mfma_bf16_supports(int L, int nl, const int32_t *widths);
+
+}  // namespace pic

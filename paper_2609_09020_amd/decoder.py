@@ -1,0 +1,238 @@
+"""Thin ctypes binding of libpic_decode.so (include/pic_decode.h).
+
+The functions ``pic_decode_create`` / ``pic_decode_run`` / ``pic_decode_query``
+/ ``pic_decode_destroy`` / ``pic_status_string`` mirror the C entry points one
+to one and only marshal arguments; every step of the decode runs in the HIP
+kernels behind them.  ``Decoder`` wraps a handle for use with torch tensors
+(torch supplies device memory and streams, nothing else).
+
+There is no fallback: if the library is missing or fails to load, every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpic_decode.so")
+
+PIC_OK, PIC_E_INVALID, PIC_E_UNSUPPORTED, PIC_E_NODEVICE, PIC_E_HIP, PIC_E_NOMEM = range(6)
+PIC_F32, PIC_BF16, PIC_U8 = 0, 1, 2
+PIC_VARIANT_AUTO, PIC_VARIANT_VALU, PIC_VARIANT_MFMA_F32, PIC_VARIANT_MFMA_BF16 = range(4)
+PIC_MAX_LEVELS, PIC_MAX_LAYERS, PIC_MAX_WIDTH, PIC_MAX_BATCH = 12, 8, 64, 65535
+PIC_FLAG_NO_CLAMP = 1
+
+VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,
+            "mfma_f32": PIC_VARIANT_MFMA_F32, "mfma_bf16": PIC_VARIANT_MFMA_BF16}
+VARIANT_NAMES = {v: k for k, v in VARIANTS.items()}
+
+# Every symbol include/pic_decode.h declares.
+EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_query",
+           "pic_decode_destroy", "pic_status_string")
+
+
+class pic_decode_desc(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32),
+                ("height", ctypes.c_int32), ("width", ctypes.c_int32),
+                ("num_levels", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("widths", ctypes.c_int32 * (PIC_MAX_LAYERS + 1)),
+                ("weight_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_uint32), ("max_batch", ctypes.c_int32),
+                ("variant", ctypes.c_int32)]
+
+
+class pic_decode_info(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("variant", ctypes.c_int32),
+                ("weights_per_image", ctypes.c_int64), ("biases_per_image", ctypes.c_int64),
+                ("device", ctypes.c_int32), ("pixels_per_wave_step", ctypes.c_int32),
+                ("kernel_name", ctypes.c_char * 64)]
+
+
+class PicError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {pic_status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libpic_decode.so; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2609_09020_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(path)
+    lib.pic_decode_create.restype = ctypes.c_int
+    lib.pic_decode_create.argtypes = [ctypes.POINTER(pic_decode_desc), ctypes.POINTER(ctypes.c_void_p)]
+    lib.pic_decode_run.restype = ctypes.c_int
+    lib.pic_decode_run.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                   ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_decode_query.restype = ctypes.c_int
+    lib.pic_decode_query.argtypes = [ctypes.c_void_p, ctypes.POINTER(pic_decode_info)]
+    lib.pic_decode_destroy.restype = None
+    lib.pic_decode_destroy.argtypes = [ctypes.c_void_p]
+    lib.pic_status_string.restype = ctypes.c_char_p
+    lib.pic_status_string.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------- C mirrors
+
+def pic_status_string(status: int) -> str:
+    return load_library().pic_status_string(int(status)).decode()
+
+
+def make_desc(height: int, width: int, widths: Sequence[int], weight_dtype: int = PIC_F32,
+              out_dtype: int = PIC_F32, flags: int = 0, max_batch: int = 1,
+              variant: int = PIC_VARIANT_AUTO) -> pic_decode_desc:
+    d = pic_decode_desc()
+    d.struct_size = ctypes.sizeof(pic_decode_desc)
+    d.height, d.width = int(height), int(width)
+    widths = [int(w) for w in widths]
+    d.num_levels = widths[0]
+    d.num_layers = len(widths) - 1
+    for i, w in enumerate(widths[:PIC_MAX_LAYERS + 1]):
+        d.widths[i] = w
+    d.weight_dtype, d.out_dtype, d.flags = int(weight_dtype), int(out_dtype), int(flags)
+    d.max_batch, d.variant = int(max_batch), int(variant)
+    return d
+
+
+def pic_decode_create(desc: pic_decode_desc) -> int:
+    """Returns the handle (an integer address); raises PicError."""
+    h = ctypes.c_void_p()
+    st = load_library().pic_decode_create(ctypes.byref(desc), ctypes.byref(h))
+    if st != PIC_OK:
+        raise PicError(st, "pic_decode_create")
+    return h.value
+
+
+def pic_decode_run(handle: int, batch: int, latent_ptrs: Sequence[int], weights_ptr: int,
+                   weights_img_stride: int, biases_ptr: int, biases_img_stride: int,
+                   out_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call; returns the status (no raise, for argument tests)."""
+    arr = (ctypes.c_void_p * max(1, len(latent_ptrs)))(*latent_ptrs)
+    return load_library().pic_decode_run(handle, batch, arr if latent_ptrs is not None else None,
+                                         weights_ptr, weights_img_stride, biases_ptr,
+                                         biases_img_stride, out_ptr, stream)
+
+
+def pic_decode_query(handle: int) -> dict:
+    info = pic_decode_info()
+    info.struct_size = ctypes.sizeof(pic_decode_info)
+    st = load_library().pic_decode_query(handle, ctypes.byref(info))
+    if st != PIC_OK:
+        raise PicError(st, "pic_decode_query")
+    return dict(variant=VARIANT_NAMES.get(info.variant, info.variant),
+                weights_per_image=info.weights_per_image, biases_per_image=info.biases_per_image,
+                device=info.device, pixels_per_wave_step=info.pixels_per_wave_step,
+                kernel_name=info.kernel_name.decode())
+
+
+def pic_decode_destroy(handle: int) -> None:
+    load_library().pic_decode_destroy(handle)
+
+
+# ------------------------------------------------------------ torch layer
+
+class Decoder:
+    """One decoder handle for a fixed image size and MLP shape.
+
+    ``run`` takes torch tensors on the handle's device: ``latents`` (L fp32
+    tensors [batch][ceil(H/2^k)][ceil(W/2^k)]), ``weights`` ([batch][nw] fp32,
+    or uint16/bfloat16 for bf16 weights; [nw] when shared), ``biases``
+    ([batch][nb] fp32 or [nb] shared).  It enqueues on torch's current stream
+    (or ``stream``) and returns ``out`` ([batch][3][H][W], float32 or uint8).
+    """
+
+    def __init__(self, height: int, width: int, widths: Sequence[int], weight_dtype: str = "f32",
+                 out_dtype: str = "f32", clamp: bool = True, max_batch: int = 1,
+                 variant: str = "auto"):
+        self.height, self.width = int(height), int(width)
+        self.widths = tuple(int(w) for w in widths)
+        self.levels = self.widths[0]
+        self.weight_dtype, self.out_dtype, self.clamp = weight_dtype, out_dtype, clamp
+        self.max_batch = int(max_batch)
+        self.desc = make_desc(height, width, self.widths,
+                              PIC_BF16 if weight_dtype == "bf16" else PIC_F32,
+                              PIC_U8 if out_dtype == "u8" else PIC_F32,
+                              0 if clamp else PIC_FLAG_NO_CLAMP, max_batch, VARIANTS[variant])
+        self.handle = pic_decode_create(self.desc)
+        self.nw = sum(self.widths[i] * self.widths[i + 1] for i in range(len(self.widths) - 1))
+        self.nb = sum(self.widths[1:])
+
+    def level_shape(self, k: int):
+        f = 1 << k
+        return (-(-self.height // f), -(-self.width // f))
+
+    def info(self) -> dict:
+        return pic_decode_query(self.handle)
+
+    def alloc_out(self, batch: int, device=None):
+        import torch
+        dt = torch.uint8 if self.out_dtype == "u8" else torch.float32
+        return torch.empty((batch, 3, self.height, self.width), dtype=dt, device=device)
+
+    def run(self, latents, weights, biases, out=None, batch: Optional[int] = None, stream=None):
+        import torch
+        batch = latents[0].shape[0] if batch is None else int(batch)
+        if len(latents) != self.levels:
+            raise ValueError(f"expected {self.levels} latent levels, got {len(latents)}")
+        dev = latents[0].device
+        if dev.type != "cuda":
+            raise ValueError("latents must be device tensors")
+        for k, t in enumerate(latents):
+            if t.dtype != torch.float32 or not t.is_contiguous() or t.device != dev:
+                raise ValueError(f"level {k}: need a contiguous float32 tensor on {dev}")
+            if tuple(t.shape[1:]) != self.level_shape(k) or t.shape[0] < batch:
+                raise ValueError(f"level {k}: shape {tuple(t.shape)}, expected "
+                                 f"[>= {batch}][{self.level_shape(k)}]")
+        wdt = (torch.uint16, torch.bfloat16, torch.int16) if self.weight_dtype == "bf16" else (torch.float32,)
+        if weights.dtype not in wdt or not weights.is_contiguous() or weights.device != dev:
+            raise ValueError(f"weights: need a contiguous {wdt[0]} tensor on {dev}")
+        if biases.dtype != torch.float32 or not biases.is_contiguous() or biases.device != dev:
+            raise ValueError(f"biases: need a contiguous float32 tensor on {dev}")
+        ws = 0 if weights.dim() == 1 else self.nw
+        bs = 0 if biases.dim() == 1 else self.nb
+        if weights.numel() < (self.nw if ws == 0 else batch * self.nw):
+            raise ValueError("weights tensor too small")
+        if biases.numel() < (self.nb if bs == 0 else batch * self.nb):
+            raise ValueError("biases tensor too small")
+        if out is None:
+            out = self.alloc_out(batch, dev)
+        want_dt = torch.uint8 if self.out_dtype == "u8" else torch.float32
+        if out.dtype != want_dt or not out.is_contiguous() or out.device != dev or \
+                tuple(out.shape[1:]) != (3, self.height, self.width) or out.shape[0] < batch:
+            raise ValueError("out: wrong dtype, shape, layout or device")
+        if stream is None:
+            stream = torch.cuda.current_stream(dev).cuda_stream
+        st = pic_decode_run(self.handle, batch, [t.data_ptr() for t in latents], weights.data_ptr(), ws,
+                            biases.data_ptr(), bs, out.data_ptr(), int(stream))
+        if st != PIC_OK:
+            raise PicError(st, "pic_decode_run")
+        return out
+
+    def close(self):
+        if getattr(self, "handle", None):
+            pic_decode_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

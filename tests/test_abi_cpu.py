@@ -1,0 +1,129 @@
+"""C ABI checks that need no GPU: the library loads, exports exactly what
+include/pic_decode.h declares, struct layouts agree with the header, and
+invalid descriptors are rejected before any device is touched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_09020_amd as pkg
+from paper_2609_09020_amd import decoder as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pic_decode.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"PIC_API\s+[\w\s\*]*?\b(pic_\w+)\s*\(", txt)))
+
+
+def test_library_loads():
+    assert os.path.exists(D.LIB_PATH), "build the library first"
+    pkg.load_library()
+
+
+def test_exports_match_header():
+    declared = _declared()
+    assert declared == sorted(D.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", D.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = sorted(l.split()[-1] for l in out.splitlines()
+                      if l.split()[-1].startswith("pic_") and " T " in l)
+    assert exported == declared
+    lib = pkg.load_library()
+    for name in declared:
+        assert hasattr(lib, name)
+
+
+def test_struct_layout_matches_header(tmp_path):
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "pic_decode.h"\n'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(pic_decode_desc),'
+                   ' offsetof(pic_decode_desc, widths), offsetof(pic_decode_desc, variant),'
+                   ' sizeof(pic_decode_info), offsetof(pic_decode_info, kernel_name),'
+                   ' offsetof(pic_decode_info, weights_per_image));return 0;}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(D.pic_decode_desc), D.pic_decode_desc.widths.offset,
+            D.pic_decode_desc.variant.offset, ctypes.sizeof(D.pic_decode_info),
+            D.pic_decode_info.kernel_name.offset, D.pic_decode_info.weights_per_image.offset]
+    assert got == want
+
+
+def test_status_strings():
+    for s in range(6):
+        assert isinstance(pkg.pic_status_string(s), str) and pkg.pic_status_string(s)
+    assert "unknown" in pkg.pic_status_string(99)
+
+
+def _create_status(_raw=None, **kw):
+    args = dict(height=64, width=64, widths=(4, 16, 16, 3))
+    args.update(kw)
+    desc = D.make_desc(**args)
+    for k, v in (_raw or {}).items():
+        setattr(desc, k, v)
+    h = ctypes.c_void_p()
+    st = pkg.load_library().pic_decode_create(ctypes.byref(desc), ctypes.byref(h))
+    if st == D.PIC_OK:
+        pkg.pic_decode_destroy(h.value)
+    else:
+        assert h.value is None
+    return st
+
+
+def _gpu_present():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+@pytest.mark.parametrize("kw", [
+    dict(height=0), dict(width=-1), dict(widths=(4, 16, 16, 4)),
+    dict(widths=(3, 16, 16, 3), _raw={"num_levels": 4}), dict(_raw={"num_layers": 0}),
+    dict(_raw={"num_layers": 9}),
+    dict(widths=(4, 65, 3)), dict(widths=(4, 0, 3)), dict(weight_dtype=2), dict(out_dtype=1),
+    dict(flags=2), dict(flags=D.PIC_FLAG_NO_CLAMP, out_dtype=D.PIC_U8), dict(max_batch=0),
+    dict(max_batch=70000), dict(variant=9), dict(height=65536, width=32768),
+    dict(widths=(13,) + (16,) * 2 + (3,)),
+])
+def test_invalid_descriptors(kw):
+    assert _create_status(**kw) == D.PIC_E_INVALID
+
+
+def test_bad_struct_size_and_null_out():
+    desc = D.make_desc(64, 64, (4, 16, 16, 3))
+    desc.struct_size = 12
+    h = ctypes.c_void_p()
+    assert pkg.load_library().pic_decode_create(ctypes.byref(desc), ctypes.byref(h)) == D.PIC_E_INVALID
+    desc = D.make_desc(64, 64, (4, 16, 16, 3))
+    assert pkg.load_library().pic_decode_create(ctypes.byref(desc), None) == D.PIC_E_INVALID
+
+
+def test_unsupported_combinations():
+    # the bf16 matrix-core family needs bf16 weights
+    assert _create_status(variant=D.PIC_VARIANT_MFMA_BF16) == D.PIC_E_UNSUPPORTED
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_nodevice_on_cpu_host():
+    assert _create_status() == D.PIC_E_NODEVICE
+    with pytest.raises(pkg.PicError) as e:
+        pkg.Decoder(64, 64, (4, 16, 16, 3))
+    assert e.value.status == D.PIC_E_NODEVICE
+
+
+def test_null_handle_is_rejected():
+    lib = pkg.load_library()
+    assert lib.pic_decode_run(None, 1, None, None, 0, None, 0, None, None) == D.PIC_E_INVALID
+    info = D.pic_decode_info()
+    info.struct_size = ctypes.sizeof(D.pic_decode_info)
+    assert lib.pic_decode_query(None, ctypes.byref(info)) == D.PIC_E_INVALID
+    lib.pic_decode_destroy(None)   # accepted

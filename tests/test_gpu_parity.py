@@ -1,0 +1,265 @@
+"""GPU parity: the HIP decode path (through the C ABI) against the CPU oracle.
+
+Bars (written here, derived in the design doc):
+  * fp32 output clamped to [0, 1]: max |gpu - oracle_f64| <= 1e-5;
+  * raw output (PIC_FLAG_NO_CLAMP): |gpu - oracle_f64| <= 1e-5 * max(1, |oracle|);
+  * 8-bit output, reference (VALU) family: identical to the oracle's binary32
+    model, which takes the same rounding decision in the same precision;
+  * 8-bit output, matrix-core family: identical to the fp64 oracle wherever
+    255 c + 1/2 lies more than 255e-5 from an integer, at most one code apart
+    inside that band;
+  * reference family raw output: equal, value for value, to the binary32
+    model for any inputs (same operations in the same order).
+Full-size workloads run on the GPU at full size in the launch configuration
+the benchmark times; the oracle checks sampled images and row strips
+(top edge, middle, bottom edge) of them.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_09020_amd import synth
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+U8_BAND = 255 * TOL
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_09020_amd as pkg
+    pkg.load_library()
+
+
+def _to_dev(inp, dev="cuda"):
+    lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
+    if inp.weights_bf16 is not None:
+        w = torch.from_numpy(inp.weights_bf16.view(np.int16)).to(dev)
+    else:
+        w = torch.from_numpy(inp.weights).to(dev)
+    b = torch.from_numpy(inp.biases).to(dev)
+    return lat, w, b
+
+
+def gpu_decode(inp, variant="auto", out_dtype="f32", clamp=True, shared=False, stream=None):
+    from paper_2609_09020_amd import Decoder
+    wdt = "bf16" if inp.weights_bf16 is not None else "f32"
+    dec = Decoder(inp.height, inp.width, inp.widths, weight_dtype=wdt, out_dtype=out_dtype,
+                  clamp=clamp, max_batch=inp.batch, variant=variant)
+    lat, w, b = _to_dev(inp)
+    if shared:
+        w, b = w[0].contiguous(), b[0].contiguous()
+    out = dec.run(lat, w, b, stream=stream)
+    torch.cuda.synchronize()
+    info = dec.info()
+    dec.close()
+    return out.cpu().numpy(), info
+
+
+def _strips(H, n=24):
+    if H <= 3 * n:
+        return [(0, H)]
+    m = H // 2
+    return [(0, n), (m - n // 2, m + n // 2), (H - n, H)]
+
+
+def _check_float(got, ref, raw, what):
+    if raw:
+        err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
+    else:
+        err = np.max(np.abs(got - ref))
+    print(f"PARITY {what}: max err {err:.3e}", flush=True)
+    assert err <= TOL, what
+
+
+def _check_u8_band(got, ref_clamped, ref_u8, what):
+    t = 255.0 * ref_clamped + 0.5
+    safe = np.abs(t - np.round(t)) > U8_BAND
+    diff = got.astype(np.int32) - ref_u8.astype(np.int32)
+    n_band = int(np.count_nonzero(diff[~safe]))
+    print(f"PARITY {what}: u8 codes differing inside the rounding band: {n_band} "
+          f"of {int(np.count_nonzero(~safe))} band samples", flush=True)
+    assert np.array_equal(got[safe], ref_u8[safe]), what
+    assert np.all(np.abs(diff) <= 1), what
+
+
+FULL = ["pic64", "kodak768", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k"]
+F32_VARIANTS = ["valu", "mfma_f32"]
+
+
+def _sample_images(batch):
+    return sorted({0, batch // 2, batch - 1}) if batch > 1 else [0]
+
+
+@pytest.mark.parametrize("variant", F32_VARIANTS)
+@pytest.mark.parametrize("name", FULL)
+def test_workload_fp32_clamped(name, variant):
+    wl = synth.WORKLOADS[name]
+    inp = synth.workload_inputs(wl)
+    got, info = gpu_decode(inp, variant=variant)
+    assert info["variant"] == variant
+    for b in _sample_images(inp.batch):
+        for rows in _strips(wl.height):
+            ref = oracle.decode_inputs(inp, out="clamped", batch_slice=slice(b, b + 1), rows=rows)
+            _check_float(got[b:b + 1, :, rows[0]:rows[1]], ref, False,
+                         f"{name} {variant} clamped img{b} rows{rows}")
+
+
+@pytest.mark.parametrize("variant", F32_VARIANTS)
+@pytest.mark.parametrize("name", ["pic64", "kodak768", "clic2048", "uhd4k"])
+def test_workload_raw(name, variant):
+    wl = synth.WORKLOADS[name]
+    inp = synth.workload_inputs(wl)
+    got, _ = gpu_decode(inp, variant=variant, clamp=False)
+    for rows in _strips(wl.height):
+        ref = oracle.decode_inputs(inp, out="raw", rows=rows)
+        _check_float(got[:, :, rows[0]:rows[1]], ref, True, f"{name} {variant} raw rows{rows}")
+
+
+@pytest.mark.parametrize("name", ["pic64", "kodak768", "kodak768_b64", "clic2048", "uhd4k"])
+def test_workload_u8_reference_bit_exact(name):
+    wl = synth.WORKLOADS[name]
+    inp = synth.workload_inputs(wl)
+    got, _ = gpu_decode(inp, variant="valu", out_dtype="u8")
+    for b in _sample_images(inp.batch):
+        for rows in _strips(wl.height):
+            ref = oracle.decode_inputs(inp, out="u8", precision="f32", batch_slice=slice(b, b + 1),
+                                       rows=rows)
+            sub = got[b:b + 1, :, rows[0]:rows[1]]
+            n = int(np.count_nonzero(sub != ref))
+            print(f"PARITY {name} valu u8 img{b} rows{rows}: {n} codes differ", flush=True)
+            assert n == 0
+
+
+@pytest.mark.parametrize("name", ["pic64", "kodak768", "kodak768_b64", "clic2048", "uhd4k"])
+def test_workload_u8_mfma_band(name):
+    wl = synth.WORKLOADS[name]
+    inp = synth.workload_inputs(wl)
+    got, _ = gpu_decode(inp, variant="mfma_f32", out_dtype="u8")
+    for b in _sample_images(inp.batch):
+        for rows in _strips(wl.height):
+            kw = dict(batch_slice=slice(b, b + 1), rows=rows)
+            refc = oracle.decode_inputs(inp, out="clamped", **kw)
+            refq = oracle.decode_inputs(inp, out="u8", **kw)
+            _check_u8_band(got[b:b + 1, :, rows[0]:rows[1]], refc, refq,
+                           f"{name} mfma_f32 img{b} rows{rows}")
+
+
+# ------------------------------------------------------------------ fuzz
+
+def _fuzz_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        H = int(rng.integers(1, 71))
+        W = int(rng.integers(1, 71))
+        L = int(rng.integers(1, 9))
+        nl = int(rng.integers(1, 5))
+        hidden = [int(rng.integers(1, 65)) for _ in range(nl - 1)]
+        widths = (L, *hidden, 3)
+        batch = int(rng.integers(1, 4))
+        cases.append((H, W, widths, batch, int(rng.integers(0, 2**31)), bool(rng.integers(0, 2))))
+    return cases
+
+
+EDGE_CASES = [
+    (1, 1, (1, 3), 1, 1, False),
+    (1, 1, (3, 5, 3), 2, 2, False),
+    (3, 5, (2, 4, 3), 1, 3, True),
+    (16, 15, (4, 16, 16, 3), 1, 4, False),
+    (16, 16, (4, 16, 16, 3), 1, 5, False),
+    (16, 17, (4, 16, 16, 3), 3, 6, False),
+    (33, 47, (12, 64, 64, 3), 2, 7, False),      # largest level count and width
+    (40, 64, (12, 17, 3), 1, 8, True),
+    (9, 70, (8, 64, 64, 64, 3), 1, 9, False),    # two hidden layers at width 64
+    (20, 30, (8, 16, 16, 16, 3), 2, 10, False),  # the paper's 4-layer width-16 shape
+    (25, 31, (5, 1, 3), 1, 11, False),
+    (7, 200, (6, 40, 3), 1, 12, False),
+]
+
+
+def _run_case(case, variant):
+    H, W, widths, batch, seed, shared = case
+    from paper_2609_09020_amd import decoder as D
+    inp = synth.make_inputs(H, W, widths[0], widths, batch=batch, seed=seed, latent="normal",
+                            latent_scale=1.5, bias="normal", shared_weights=shared)
+    nl = len(widths) - 1
+    if variant == "mfma_f32" and not (2 <= nl <= 4):
+        with pytest.raises(D.PicError) as e:
+            gpu_decode(inp, variant=variant)
+        assert e.value.status == D.PIC_E_UNSUPPORTED
+        return None
+    got, _ = gpu_decode(inp, variant=variant, clamp=False, shared=shared)
+    ref = oracle.decode_inputs(inp, out="raw")
+    _check_float(got, ref, True, f"fuzz {case} {variant}")
+    return inp, got
+
+
+@pytest.mark.parametrize("variant", F32_VARIANTS)
+@pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(24, 2024), ids=str)
+def test_fuzz_raw(case, variant):
+    _run_case(case, variant)
+
+
+@pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(12, 77), ids=str)
+def test_reference_family_matches_binary32_model(case):
+    r = _run_case(case, "valu")
+    inp, got = r
+    ref32 = oracle.decode_inputs(inp, out="raw", precision="f32")
+    n = int(np.count_nonzero(got != ref32))
+    assert n == 0, f"{n} values differ from the binary32 model"
+
+
+def test_shared_weights_stride_zero_matches_repeated():
+    inp = synth.make_inputs(37, 53, 6, (6, 24, 24, 3), batch=3, seed=5, latent="normal",
+                            bias="normal", shared_weights=True)
+    for variant in F32_VARIANTS:
+        a, _ = gpu_decode(inp, variant=variant, clamp=False, shared=True)
+        b, _ = gpu_decode(inp, variant=variant, clamp=False, shared=False)
+        assert np.array_equal(a, b)
+
+
+def test_batch_zero_enqueues_nothing():
+    from paper_2609_09020_amd import Decoder
+    inp = synth.make_inputs(8, 8, 2, (2, 4, 3), batch=1, seed=0)
+    lat, w, b = _to_dev(inp)
+    dec = Decoder(8, 8, (2, 4, 3), max_batch=1)
+    out = torch.full((1, 3, 8, 8), 7.0, device="cuda")
+    dec.run(lat, w, b, out=out, batch=0)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+
+
+def test_runs_on_caller_stream():
+    inp = synth.workload_inputs(synth.WORKLOADS["kodak768"])
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        got, _ = gpu_decode(inp, variant="mfma_f32", stream=s.cuda_stream)
+    ref, _ = gpu_decode(inp, variant="mfma_f32")
+    assert np.array_equal(got, ref)
+
+
+def test_run_rejects_bad_arguments_before_launch():
+    from paper_2609_09020_amd import decoder as D
+    inp = synth.make_inputs(8, 8, 2, (2, 4, 3), batch=2, seed=0)
+    lat, w, b = _to_dev(inp)
+    dec = D.Decoder(8, 8, (2, 4, 3), max_batch=2)
+    out = dec.alloc_out(2, "cuda")
+    ptrs = [t.data_ptr() for t in lat]
+    h = dec.handle
+    run = D.pic_decode_run
+    assert run(h, 3, ptrs, w.data_ptr(), 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, -1, ptrs, w.data_ptr(), 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, ptrs, 0, 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, ptrs, w.data_ptr(), 19, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, ptrs, w.data_ptr(), 20, b.data_ptr(), -1, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, ptrs, w.data_ptr() + 2, 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, [ptrs[0], 0], w.data_ptr(), 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_E_INVALID
+    assert run(h, 2, ptrs, w.data_ptr(), 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_OK
+    torch.cuda.synchronize()
+    dec.close()

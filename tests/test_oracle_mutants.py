@@ -34,8 +34,9 @@ MUTANTS = [
      "((uint8_t *)out)[o] = (uint8_t)floor(255.0 * cl);"),
     ("no_upper_clamp", "double cl = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);",
      "double cl = v < 0.0 ? 0.0 : v;"),
-    ("wrong_output_plane", "size_t o = (((size_t)b * 3 + c) * H + y) * (size_t)W + x;\n                double v",
-     "size_t o = (((size_t)b * 3 + (2 - c)) * H + y) * (size_t)W + x;\n                double v"),
+    ("wrong_output_plane",
+     "size_t o = (((size_t)b * 3 + c) * R + (y - y_begin)) * (size_t)W + x;\n                double v",
+     "size_t o = (((size_t)b * 3 + (2 - c)) * R + (y - y_begin)) * (size_t)W + x;\n                double v"),
     ("f32_model_no_bias", "float acc = bias[bo + j];", "float acc = 0.0f;"),
     ("f32_model_transposed", "long idx = wo + (long)j * fin + i;\n                        float wv",
      "long idx = wo + (long)i * fout + j;\n                        float wv"),

@@ -26,3 +26,13 @@ def test_rejects_bad_arguments(orc):
         orc.decode(lat, w, b, (2, 4, 4), 4, 4)
     with pytest.raises(ValueError):       # level 1 has the wrong shape
         orc.decode([lat[0], np.zeros((1, 3, 2), np.float32)], w, b, (2, 4, 3), 4, 4)
+
+
+def test_row_range_matches_full_decode(orc):
+    import numpy as np
+    from paper_2609_09020_amd import synth
+    inp = synth.make_inputs(37, 29, 4, (4, 9, 3), batch=2, seed=1, latent="normal", bias="normal")
+    full = orc.decode_inputs(inp, out="raw")
+    for rows in ((0, 37), (0, 1), (36, 37), (5, 20)):
+        part = orc.decode_inputs(inp, out="raw", rows=rows)
+        assert np.array_equal(full[:, :, rows[0]:rows[1]], part)
