@@ -1,0 +1,391 @@
+// fp32 matrix-core decode kernel (v_mfma_f32_16x16x4_f32), shared by the
+// k_mfma_f32_nh*.hip translation units that instantiate it.
+//
+// What it computes (PIC, Sec. 3.1 and App. A): per pixel, every latent level
+// upsampled bilinearly (half-pixel centres, edge replication, scale 2^k) into
+// an L-vector, then the synthesis MLP (ReLU between layers, none after the
+// last), clamp to [0, 1], optional 8-bit quantisation.
+//
+// Work decomposition
+//   A workgroup (4 wavefronts) owns one image and walks tiles of 8 rows x 64
+//   columns of it.  Per tile it stages, for every level, the window of latent
+//   texels the tile's pixels sample (with the one-texel halo the bilinear taps
+//   need) into LDS with coalesced loads; each wavefront then evaluates two
+//   rows of the tile, 16 consecutive pixels at a time.
+//
+// Matrix-core mapping (lane l, lane group g = l / 16, i = l % 16)
+//   v_mfma_f32_16x16x4_f32 takes A[i][g] and B[g][i] from lane l and returns
+//   D[4g + r][i] in register r of lane l.  A layer is D = W * H^T + bias with
+//   16 output neurons on the rows of a block and the 16 pixels on the columns.
+//   Row 4g + r of output block ob holds neuron 16 ob + 4 r + g, so register r
+//   of block nb, read across the lane groups, holds neurons 16 nb + 4 r + g:
+//   exactly the B operand of K step (nb, r) of the next layer, with K index g.
+//   Layers therefore chain through the accumulators with no data movement.
+//   K steps run in increasing input order (inputs 4j .. 4j+3 at step j), and a
+//   partially filled last block keeps its n valid inputs on steps < ceil(n/4)
+//   so steps over padding are skipped.  Lane group g of the first layer's B
+//   operand supplies level 4 s + g of the lane's pixel at K step s.
+//
+//   Weights are gathered once per workgroup into LDS in that operand layout
+//   (zero padded), then held in VGPRs for the workgroup's lifetime; biases
+//   (accumulator layout) and the output layer's weights are read from LDS per
+//   16-pixel group.  The output layer (3 neurons) runs on the vector ALU: each
+//   lane forms partial sums over the 4 NB hidden values it holds and two
+//   cross-lane butterflies add the four lane groups.
+#pragma once
+
+#include "pic_internal.h"
+
+namespace pic {
+namespace mfma_f32 {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int TH = 8;    // tile rows (two per wavefront)
+constexpr int TW = 64;   // tile columns (four 16-pixel groups per row)
+
+// Latent box staged per level for one tile.  A tile's pixels o0 .. o1 along
+// an axis sample source indices floor(src(o0)) .. floor(src(o1)) + 1, at most
+// ceil((n - 1) / 2^k) + 2 of them; the box holds that many (rounded up by one)
+// starting at floor(src(o0)).  Indices past the grid are staged as the grid's
+// last sample, which is exactly the edge replication of the upsample, so every
+// pixel's second tap is at +1 (column) and +pitch (row).
+__host__ __device__ constexpr int box_dim(int n, int k) { return ((n - 1 + (1 << k) - 1) >> k) + 3; }
+__host__ __device__ constexpr int box_rows(int k) { return box_dim(TH, k); }
+__host__ __device__ constexpr int box_pitch(int k) { return box_dim(TW, k); }
+__host__ __device__ constexpr int box_floats(int k) { return box_rows(k) * box_pitch(k); }
+__host__ __device__ constexpr int box_offset(int k) { return k == 0 ? 0 : box_offset(k - 1) + box_floats(k - 1); }
+
+template <int NB, int NH, int LS, int KSH>
+struct Layout {
+    static constexpr int W1A = 0;                                   // [NB][LS][64]
+    static constexpr int WHA = W1A + NB * LS * 64;                  // [NH][NB][KSH][64]
+    static constexpr int B1 = WHA + NH * NB * KSH * 64;             // [NB][64][4]
+    static constexpr int BH = B1 + NB * 64 * 4;                     // [NH][NB][64][4]
+    static constexpr int W3 = BH + NH * NB * 64 * 4;                // [NB][4 r][4 g][4 c]
+    static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent windows
+    static constexpr int SIZE = LAT + box_offset(4 * LS);
+};
+
+__device__ __forceinline__ float pow2_neg(int k) { return __int_as_float((127 - k) << 23); }
+
+// floor of the clamped source coordinate max((o + 1/2) 2^-k - 1/2, 0).
+__device__ __forceinline__ int src_floor(int o, float inv)
+{
+    const float s = ((float)o + 0.5f) * inv - 0.5f;
+    return s <= 0.0f ? 0 : (int)s;
+}
+
+__device__ __forceinline__ float load_weight(const DecodeParams &p, int64_t idx)
+{
+    if (p.weights_bf16)
+        return __uint_as_float((uint32_t) static_cast<const uint16_t *>(p.weights)[idx] << 16);
+    return static_cast<const float *>(p.weights)[idx];
+}
+
+// Neuron on row `row` of an output block; the map is its own inverse.
+__device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row >> 2); }
+
+// max(x, 0) for a non-NaN float as one integer max: non-negative floats order
+// like their bit patterns, negative ones (sign bit set) are negative integers.
+__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
+
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+// Sum of x over the four 16-lane rows of the wavefront, in every lane:
+// permlane16_swap pairs rows (0,1) and (2,3), permlane32_swap pairs the halves;
+// the two outputs of each swap hold both members of the pair.
+__device__ __forceinline__ float row_sum(float x)
+{
+    const unsigned xi = __float_as_uint(x);
+    const u32x2 a = __builtin_amdgcn_permlane16_swap(xi, xi, false, false);
+    const float s = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned si = __float_as_uint(s);
+    const u32x2 c = __builtin_amdgcn_permlane32_swap(si, si, false, false);
+    return __uint_as_float(c[0]) + __uint_as_float(c[1]);
+}
+
+// NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: K steps of
+// the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
+// 4 KSH and up are padding and skipped).
+template <int NB, int NH, int LS, int KSH>
+__global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int blocks_per_image,
+                                                       int tiles_x, int tiles)
+{
+    static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
+    using LY = Layout<NB, NH, LS, KSH>;
+    __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, col = lane & 15;
+    const int b = blockIdx.x / blocks_per_image;
+    const int blk = blockIdx.x - b * blocks_per_image;
+    const int L = p.L;
+    const int64_t wbase = (int64_t)b * p.w_stride;
+    const int64_t bbase = (int64_t)b * p.b_stride;
+
+    // ---- stage this image's parameters into LDS in operand layouts
+    {
+        const int N1 = p.widths[1];
+        for (int s = tid; s < NB * LS * 64; s += kThreads) {          // layer 1, A layout
+            const int ln = s & 63, step = (s >> 6) % LS, ob = (s >> 6) / LS;
+            const int out = 16 * ob + row_neuron(ln & 15), in = 4 * step + (ln >> 4);
+            lds[LY::W1A + s] = (out < N1 && in < L) ? load_weight(p, wbase + p.woff[0] + out * L + in) : 0.0f;
+        }
+        for (int s = tid; s < NH * NB * KSH * 64; s += kThreads) {   // hidden layers, A layout
+            const int ln = s & 63, ks = (s >> 6) % KSH, ob = ((s >> 6) / KSH) % NB;
+            const int h = (s >> 6) / (KSH * NB);
+            const int fin = p.widths[1 + h], fout = p.widths[2 + h];
+            const int out = 16 * ob + row_neuron(ln & 15);
+            const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
+            lds[LY::WHA + s] = (out < fout && in < fin)
+                                   ? load_weight(p, wbase + p.woff[1 + h] + out * fin + in) : 0.0f;
+        }
+        for (int s = tid; s < (1 + NH) * NB * 64 * 4; s += kThreads) { // biases, accumulator layout
+            const int r = s & 3, ln = (s >> 2) & 63, ob = (s >> 8) % NB, h = (s >> 8) / NB;
+            const int n = 16 * ob + 4 * r + (ln >> 4), fout = p.widths[1 + h];
+            lds[LY::B1 + s] = n < fout ? p.biases[bbase + p.boff[h] + n] : 0.0f;
+        }
+        const int NL = p.widths[NH + 1];
+        for (int s = tid; s < NB * 64; s += kThreads) {                // output layer [ob][r][g][c]
+            const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
+            const int n = 16 * ob + 4 * r + gg;
+            lds[LY::W3 + s] = (c < 3 && n < NL) ? load_weight(p, wbase + p.woff[NH + 1] + c * NL + n) : 0.0f;
+        }
+    }
+    const float b3_0 = p.biases[bbase + p.boff[NH + 1] + 0];
+    const float b3_1 = p.biases[bbase + p.boff[NH + 1] + 1];
+    const float b3_2 = p.biases[bbase + p.boff[NH + 1] + 2];
+    __syncthreads();
+
+    float w1[NB][LS];
+#pragma unroll
+    for (int ob = 0; ob < NB; ++ob)
+#pragma unroll
+        for (int s = 0; s < LS; ++s)
+            w1[ob][s] = lds[LY::W1A + (ob * LS + s) * 64 + lane];
+    float wh[NH > 0 ? NH : 1][NB][KSH];
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+#pragma unroll
+        for (int ob = 0; ob < NB; ++ob)
+#pragma unroll
+            for (int ks = 0; ks < KSH; ++ks)
+                wh[h][ob][ks] = lds[LY::WHA + ((h * NB + ob) * KSH + ks) * 64 + lane];
+
+    // ---- per-lane level constants for the first layer's B operand
+    // Lanes whose level 4 s + g does not exist sample level 0 instead: their
+    // first-layer weights are zero, so the (finite) value is ignored.
+    float inv[LS];
+    int loff[LS], pitch[LS];
+#pragma unroll
+    for (int s = 0; s < LS; ++s) {
+        const int k = 4 * s + g;
+        const int kk = k < L ? k : 0;
+        inv[s] = pow2_neg(kk);
+        loff[s] = LY::LAT + box_offset(kk);
+        pitch[s] = box_pitch(kk);
+    }
+
+    const int H = p.H, W = p.W;
+    const int64_t plane = (int64_t)H * W;
+    // Lane group g (< 3) stores channel g; lane group 0 carries the output
+    // biases in its partial sums.
+    const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
+    const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
+    constexpr int KS1 = KSH < 4 * NB ? KSH : 4 * NB;   // live registers of a hidden activation
+
+    for (int t = blk; t < tiles; t += blocks_per_image) {
+        const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
+        const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
+
+        __syncthreads();   // every wavefront is done with the previous tile's boxes
+#pragma unroll
+        for (int k = 0; k < 4 * LS; ++k) {
+            if (k < L) {
+                const float iv = pow2_neg(k);
+                const int hk = p.hk[k], wk = p.wk[k];
+                const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
+                const float *src = p.lat[k] + (int64_t)b * hk * wk;
+                float *dst = lds + LY::LAT + box_offset(k);
+                const int n = box_floats(k), pc = box_pitch(k);   // constants once unrolled
+#pragma unroll
+                for (int i0 = 0; i0 < n; i0 += kThreads) {
+                    const int i = i0 + tid;
+                    if (i0 + kThreads <= n || i < n) {
+                        const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
+                        dst[i] = src[(int64_t)r * wk + c];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // Column part of every level's taps for the tile's four 16-pixel columns.
+        int coff[LS][4];
+        float clx[LS][4];
+        int rbase[LS];
+#pragma unroll
+        for (int s = 0; s < LS; ++s) {
+            const int rx = src_floor(tx0, inv[s]);
+            rbase[s] = src_floor(ty0, inv[s]);
+#pragma unroll
+            for (int cg = 0; cg < 4; ++cg) {
+                const int x = min(tx0 + 16 * cg + col, tx1);
+                const float sx = fmaxf(((float)x + 0.5f) * inv[s] - 0.5f, 0.0f);
+                const int x0 = (int)sx;
+                clx[s][cg] = sx - (float)x0;
+                coff[s][cg] = loff[s] + x0 - rx;
+            }
+        }
+
+#pragma unroll 1
+        for (int rr = 0; rr < 2; ++rr) {
+            const int y = ty0 + 2 * wave + rr;
+            if (y > ty1)
+                break;   // wave-uniform: the row lies below the image
+            int roff[LS];
+            float rly[LS];
+#pragma unroll
+            for (int s = 0; s < LS; ++s) {
+                const float sy = fmaxf(((float)y + 0.5f) * inv[s] - 0.5f, 0.0f);
+                const int y0 = (int)sy;
+                rly[s] = sy - (float)y0;
+                roff[s] = (y0 - rbase[s]) * pitch[s];
+            }
+            const int64_t orow = obase + (int64_t)y * W + tx0 + col;
+
+#pragma unroll
+            for (int cg = 0; cg < 4; ++cg) {
+                if (tx0 + 16 * cg > tx1)
+                    break;   // wave-uniform: the column group lies right of the image
+
+                // layer 1: K = levels, B operand = upsampled pyramid
+                f32x4 d[NB];
+#pragma unroll
+                for (int ob = 0; ob < NB; ++ob)
+                    d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + (ob * 64 + lane) * 4]);
+#pragma unroll
+                for (int s = 0; s < LS; ++s) {
+                    const float *q0 = lds + roff[s] + coff[s][cg];
+                    const float *q1 = q0 + pitch[s];
+                    const float a = q0[0], bq = q0[1], c = q1[0], e = q1[1];
+                    const float lx = clx[s][cg];
+                    const float top = __builtin_fmaf(lx, bq - a, a);
+                    const float bot = __builtin_fmaf(lx, e - c, c);
+                    const float u = __builtin_fmaf(rly[s], bot - top, top);
+#pragma unroll
+                    for (int ob = 0; ob < NB; ++ob)
+                        d[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[ob][s], u, d[ob], 0, 0, 0);
+                }
+#pragma unroll
+                for (int ks = 0; ks < KS1; ++ks)
+                    d[ks >> 2][ks & 3] = relu(d[ks >> 2][ks & 3]);
+
+                // hidden layers
+#pragma unroll
+                for (int h = 0; h < NH; ++h) {
+                    f32x4 e[NB];
+#pragma unroll
+                    for (int ob = 0; ob < NB; ++ob)
+                        e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BH + ((h * NB + ob) * 64 + lane) * 4]);
+#pragma unroll
+                    for (int ks = 0; ks < KSH; ++ks)
+#pragma unroll
+                        for (int ob = 0; ob < NB; ++ob)
+                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wh[h][ob][ks], d[ks >> 2][ks & 3], e[ob],
+                                                                         0, 0, 0);
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks)
+                        d[ks >> 2][ks & 3] = relu(e[ks >> 2][ks & 3]);
+                }
+
+                // output layer on the vector ALU: partial sums over this lane's
+                // live hidden values, then a sum over the four lane groups
+                float o0 = ob0, o1 = ob1, o2 = ob2;
+#pragma unroll
+                for (int ks = 0; ks < KS1; ++ks) {
+                    const f32x4 w3 = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + (ks * 4 + g) * 4]);
+                    const float hv = d[ks >> 2][ks & 3];
+                    o0 = __builtin_fmaf(w3[0], hv, o0);
+                    o1 = __builtin_fmaf(w3[1], hv, o1);
+                    o2 = __builtin_fmaf(w3[2], hv, o2);
+                }
+                o0 = row_sum(o0);
+                o1 = row_sum(o1);
+                o2 = row_sum(o2);
+
+                if (g < 3 && tx0 + 16 * cg + col <= tx1) {
+                    const float v = g == 0 ? o0 : (g == 1 ? o1 : o2);
+                    const int64_t o = orow + 16 * cg;
+                    if (p.out_kind == OUT_RAW_F32) {
+                        static_cast<float *>(p.out)[o] = v;
+                    } else {
+                        const float cl = fminf(fmaxf(v, 0.0f), 1.0f);
+                        if (p.out_kind == OUT_CLAMPED_F32)
+                            static_cast<float *>(p.out)[o] = cl;
+                        else
+                            static_cast<uint8_t *>(p.out)[o] = (uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f));
+                    }
+                }
+            }
+        }
+    }
+}
+
+int hidden_blocks(int nl, const int32_t *widths);
+
+template <int NB, int NH, int LS, int KSH>
+hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+{
+    const int tiles_x = (p.W + TW - 1) / TW, tiles_y = (p.H + TH - 1) / TH;
+    const int tiles = tiles_x * tiles_y;
+    // As many workgroups as can be resident at once, split evenly over images.
+    static int occ = 0;
+    if (occ == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mfma_f32<NB, NH, LS, KSH>, kThreads, 0) != hipSuccess ||
+            n < 1)
+            n = 2;
+        occ = n;
+    }
+    const int target = occ * num_cus;
+    int bpi = (target + p.batch - 1) / p.batch;
+    bpi = bpi < 1 ? 1 : (bpi > tiles ? tiles : bpi);
+    const int64_t nblocks = (int64_t)bpi * p.batch;
+    if (nblocks > 0x7fffffff)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_mfma_f32<NB, NH, LS, KSH>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
+                       tiles_x, tiles);
+    return hipGetLastError();
+}
+
+// Hidden K steps the shape needs: ceil(width / 4) of the widest hidden input.
+int hidden_ksteps(int nl, const int32_t *widths);
+
+template <int NH>
+hipError_t launch_nh(const DecodeParams &p, hipStream_t s, int num_cus)
+{
+    const int NB = hidden_blocks(p.nl, p.widths);
+    const int LS = (p.L + 3) / 4;
+    // Width 33..40 (three blocks, last one half used) gets its own K-step
+    // count; every other width runs all 4 NB steps over zero padding.
+    const bool k10 = NH > 0 && NB == 3 && hidden_ksteps(p.nl, p.widths) <= 10;
+#define PIC_CASE(nb, ls, ksh) \
+    if (NB == nb && LS == ls && (ksh != 4 * nb) == (nb == 3 && k10)) return launch<nb, NH, ls, ksh>(p, s, num_cus);
+    PIC_CASE(1, 1, 4) PIC_CASE(1, 2, 4) PIC_CASE(1, 3, 4)
+    PIC_CASE(2, 1, 8) PIC_CASE(2, 2, 8) PIC_CASE(2, 3, 8)
+    PIC_CASE(3, 1, 12) PIC_CASE(3, 2, 12) PIC_CASE(3, 3, 12)
+    PIC_CASE(4, 1, 16) PIC_CASE(4, 2, 16) PIC_CASE(4, 3, 16)
+    if constexpr (NH > 0) {
+        PIC_CASE(3, 1, 10) PIC_CASE(3, 2, 10) PIC_CASE(3, 3, 10)
+    }
+#undef PIC_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace mfma_f32
+}  // namespace pic
