@@ -1,0 +1,181 @@
+// Device pieces shared by the matrix-core decode kernels: tile geometry, the
+// LDS latent boxes, the bilinear upsample from them, the cross-lane sums of
+// the output layer and the epilogue.
+//
+// The upsample (PIC, Sec. 3.1): level k of an H x W image is a grid of
+// ceil(H / 2^k) x ceil(W / 2^k) samples; output pixel (y, x) samples it at
+// source coordinate max((y + 1/2) 2^-k - 1/2, 0) (and likewise for x), from
+// the two neighbouring samples of each axis, the upper one clamped to the
+// grid (edge replication).
+#pragma once
+
+#include "pic_internal.h"
+
+namespace pic {
+namespace tile {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int TH = 8;    // tile rows (two per wavefront)
+constexpr int TW = 64;   // tile columns (four 16-pixel groups per row)
+
+// Latent box staged per level for one tile.  A tile's pixels o0 .. o1 along
+// an axis sample source indices floor(src(o0)) .. floor(src(o1)) + 1, at most
+// ceil((n - 1) / 2^k) + 2 of them; the box holds that many (rounded up by one)
+// starting at floor(src(o0)).  Indices past the grid are staged as the grid's
+// last sample, which is exactly the edge replication of the upsample, so every
+// pixel's second tap is at +1 (column) and +pitch (row).
+__host__ __device__ constexpr int box_dim(int n, int k) { return ((n - 1 + (1 << k) - 1) >> k) + 3; }
+__host__ __device__ constexpr int box_rows(int k) { return box_dim(TH, k); }
+__host__ __device__ constexpr int box_pitch(int k) { return box_dim(TW, k); }
+__host__ __device__ constexpr int box_floats(int k) { return box_rows(k) * box_pitch(k); }
+__host__ __device__ constexpr int box_offset(int k) { return k == 0 ? 0 : box_offset(k - 1) + box_floats(k - 1); }
+
+__device__ __forceinline__ float pow2_neg(int k) { return __int_as_float((127 - k) << 23); }
+
+// floor of the clamped source coordinate max((o + 1/2) 2^-k - 1/2, 0).
+__device__ __forceinline__ int src_floor(int o, float inv)
+{
+    const float s = ((float)o + 0.5f) * inv - 0.5f;
+    return s <= 0.0f ? 0 : (int)s;
+}
+
+// Weight element idx of the image's parameter block, as fp32.
+__device__ __forceinline__ float load_weight(const DecodeParams &p, int64_t idx)
+{
+    if (p.weights_bf16)
+        return __uint_as_float((uint32_t) static_cast<const uint16_t *>(p.weights)[idx] << 16);
+    return static_cast<const float *>(p.weights)[idx];
+}
+
+// max(x, 0) for a non-NaN float as one integer max: non-negative floats order
+// like their bit patterns, negative ones (sign bit set) are negative integers.
+__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
+
+// Sum of x over the four 16-lane rows of the wavefront, in every lane:
+// permlane16_swap pairs rows (0,1) and (2,3), permlane32_swap pairs the halves;
+// the two outputs of each swap hold both members of the pair.
+__device__ __forceinline__ float row_sum(float x)
+{
+    const unsigned xi = __float_as_uint(x);
+    const u32x2 a = __builtin_amdgcn_permlane16_swap(xi, xi, false, false);
+    const float s = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned si = __float_as_uint(s);
+    const u32x2 c = __builtin_amdgcn_permlane32_swap(si, si, false, false);
+    return __uint_as_float(c[0]) + __uint_as_float(c[1]);
+}
+
+// Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
+// (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
+template <int KMAX>
+__device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, int b, int ty0, int tx0, int tid)
+{
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        if (k < p.L) {
+            const float iv = pow2_neg(k);
+            const int hk = p.hk[k], wk = p.wk[k];
+            const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
+            const float *src = p.lat[k] + (int64_t)b * hk * wk;
+            float *dst = lat + box_offset(k);
+            const int n = box_floats(k), pc = box_pitch(k);   // constants once unrolled
+#pragma unroll
+            for (int i0 = 0; i0 < n; i0 += kThreads) {
+                const int i = i0 + tid;
+                if (i0 + kThreads <= n || i < n) {
+                    const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
+                    dst[i] = src[(int64_t)r * wk + c];
+                }
+            }
+        }
+    }
+}
+
+// One lane's view of one level for the current tile: where its box starts in
+// LDS, its pitch, and the horizontal tap offsets / weights of the tile's four
+// 16-pixel column groups.
+struct LaneLevel {
+    float inv;        // 2^-k
+    int loff;         // LDS offset of the level's box (floats)
+    int pitch;        // box row pitch (floats)
+    int rbase;        // first source row of the box
+    int coff[4];      // loff + first-tap column - first box column, per column group
+    float clx[4];     // horizontal lerp weight, per column group
+};
+
+__device__ __forceinline__ void lane_level_init(LaneLevel &lv, int k, int lat_base)
+{
+    lv.inv = pow2_neg(k);
+    lv.loff = lat_base + box_offset(k);
+    lv.pitch = box_pitch(k);
+}
+
+__device__ __forceinline__ void lane_level_tile(LaneLevel &lv, int ty0, int tx0, int tx1, int col)
+{
+    const int rx = src_floor(tx0, lv.inv);
+    lv.rbase = src_floor(ty0, lv.inv);
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) {
+        const int x = min(tx0 + 16 * cg + col, tx1);
+        const float sx = fmaxf(((float)x + 0.5f) * lv.inv - 0.5f, 0.0f);
+        const int x0 = (int)sx;
+        lv.clx[cg] = sx - (float)x0;
+        lv.coff[cg] = lv.loff + x0 - rx;
+    }
+}
+
+// Vertical part for output row y: box row offset of the first tap and weight.
+__device__ __forceinline__ void lane_level_row(const LaneLevel &lv, int y, int &roff, float &ly)
+{
+    const float sy = fmaxf(((float)y + 0.5f) * lv.inv - 0.5f, 0.0f);
+    const int y0 = (int)sy;
+    ly = sy - (float)y0;
+    roff = (y0 - lv.rbase) * lv.pitch;
+}
+
+// Bilinear sample from the box: taps at +0, +1, +pitch, +pitch+1.
+__device__ __forceinline__ float lane_level_sample(const float *lds, const LaneLevel &lv, int roff, float ly, int cg)
+{
+    const float *q0 = lds + roff + lv.coff[cg];
+    const float *q1 = q0 + lv.pitch;
+    const float a = q0[0], b = q0[1], c = q1[0], d = q1[1];
+    const float lx = lv.clx[cg];
+    const float top = __builtin_fmaf(lx, b - a, a);
+    const float bot = __builtin_fmaf(lx, d - c, c);
+    return __builtin_fmaf(ly, bot - top, top);
+}
+
+// Write one output value (lane group g < 3 writes channel g).
+__device__ __forceinline__ void store_out(const DecodeParams &p, int64_t o, float v)
+{
+    if (p.out_kind == OUT_RAW_F32) {
+        static_cast<float *>(p.out)[o] = v;
+    } else {
+        const float cl = fminf(fmaxf(v, 0.0f), 1.0f);
+        if (p.out_kind == OUT_CLAMPED_F32)
+            static_cast<float *>(p.out)[o] = cl;
+        else
+            static_cast<uint8_t *>(p.out)[o] = (uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f));
+    }
+}
+
+// Grid size for a persistent kernel: as many workgroups as fit at once,
+// split evenly over the images (at least one, at most one per tile).
+template <typename K>
+int blocks_per_image(K kernel, const DecodeParams &p, int num_cus, int tiles, int &occ_cache)
+{
+    if (occ_cache == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kThreads, 0) != hipSuccess || n < 1)
+            n = 2;
+        occ_cache = n;
+    }
+    int bpi = (occ_cache * num_cus + p.batch - 1) / p.batch;
+    return bpi < 1 ? 1 : (bpi > tiles ? tiles : bpi);
+}
+
+}  // namespace tile
+}  // namespace pic

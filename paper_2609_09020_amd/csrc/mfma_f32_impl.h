@@ -8,10 +8,10 @@
 //
 // Work decomposition
 //   A workgroup (4 wavefronts) owns one image and walks tiles of 8 rows x 64
-//   columns of it.  Per tile it stages, for every level, the window of latent
-//   texels the tile's pixels sample (with the one-texel halo the bilinear taps
-//   need) into LDS with coalesced loads; each wavefront then evaluates two
-//   rows of the tile, 16 consecutive pixels at a time.
+//   columns of it.  Per tile it stages, for every level, the box of latent
+//   texels the tile's pixels sample into LDS with coalesced loads
+//   (decode_common.h); each wavefront then evaluates two rows of the tile,
+//   16 consecutive pixels at a time.
 //
 // Matrix-core mapping (lane l, lane group g = l / 16, i = l % 16)
 //   v_mfma_f32_16x16x4_f32 takes A[i][g] and B[g][i] from lane l and returns
@@ -30,33 +30,20 @@
 //   (zero padded), then held in VGPRs for the workgroup's lifetime; biases
 //   (accumulator layout) and the output layer's weights are read from LDS per
 //   16-pixel group.  The output layer (3 neurons) runs on the vector ALU: each
-//   lane forms partial sums over the 4 NB hidden values it holds and two
-//   cross-lane butterflies add the four lane groups.
+//   lane forms partial sums over the hidden values it holds and two cross-lane
+//   swaps add the four lane groups.
+//
+//   fp32 matrix and vector instructions share a SIMD's issue capacity, so the
+//   per-group vector work is kept small: fixed-offset bilinear taps, ReLU as
+//   one integer max, no padding registers touched.
 #pragma once
 
-#include "pic_internal.h"
+#include "decode_common.h"
 
 namespace pic {
 namespace mfma_f32 {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-constexpr int TH = 8;    // tile rows (two per wavefront)
-constexpr int TW = 64;   // tile columns (four 16-pixel groups per row)
-
-// Latent box staged per level for one tile.  A tile's pixels o0 .. o1 along
-// an axis sample source indices floor(src(o0)) .. floor(src(o1)) + 1, at most
-// ceil((n - 1) / 2^k) + 2 of them; the box holds that many (rounded up by one)
-// starting at floor(src(o0)).  Indices past the grid are staged as the grid's
-// last sample, which is exactly the edge replication of the upsample, so every
-// pixel's second tap is at +1 (column) and +pitch (row).
-__host__ __device__ constexpr int box_dim(int n, int k) { return ((n - 1 + (1 << k) - 1) >> k) + 3; }
-__host__ __device__ constexpr int box_rows(int k) { return box_dim(TH, k); }
-__host__ __device__ constexpr int box_pitch(int k) { return box_dim(TW, k); }
-__host__ __device__ constexpr int box_floats(int k) { return box_rows(k) * box_pitch(k); }
-__host__ __device__ constexpr int box_offset(int k) { return k == 0 ? 0 : box_offset(k - 1) + box_floats(k - 1); }
+using namespace tile;
 
 template <int NB, int NH, int LS, int KSH>
 struct Layout {
@@ -65,47 +52,12 @@ struct Layout {
     static constexpr int B1 = WHA + NH * NB * KSH * 64;             // [NB][64][4]
     static constexpr int BH = B1 + NB * 64 * 4;                     // [NH][NB][64][4]
     static constexpr int W3 = BH + NH * NB * 64 * 4;                // [NB][4 r][4 g][4 c]
-    static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent windows
+    static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent boxes
     static constexpr int SIZE = LAT + box_offset(4 * LS);
 };
 
-__device__ __forceinline__ float pow2_neg(int k) { return __int_as_float((127 - k) << 23); }
-
-// floor of the clamped source coordinate max((o + 1/2) 2^-k - 1/2, 0).
-__device__ __forceinline__ int src_floor(int o, float inv)
-{
-    const float s = ((float)o + 0.5f) * inv - 0.5f;
-    return s <= 0.0f ? 0 : (int)s;
-}
-
-__device__ __forceinline__ float load_weight(const DecodeParams &p, int64_t idx)
-{
-    if (p.weights_bf16)
-        return __uint_as_float((uint32_t) static_cast<const uint16_t *>(p.weights)[idx] << 16);
-    return static_cast<const float *>(p.weights)[idx];
-}
-
 // Neuron on row `row` of an output block; the map is its own inverse.
 __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row >> 2); }
-
-// max(x, 0) for a non-NaN float as one integer max: non-negative floats order
-// like their bit patterns, negative ones (sign bit set) are negative integers.
-__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
-
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-
-// Sum of x over the four 16-lane rows of the wavefront, in every lane:
-// permlane16_swap pairs rows (0,1) and (2,3), permlane32_swap pairs the halves;
-// the two outputs of each swap hold both members of the pair.
-__device__ __forceinline__ float row_sum(float x)
-{
-    const unsigned xi = __float_as_uint(x);
-    const u32x2 a = __builtin_amdgcn_permlane16_swap(xi, xi, false, false);
-    const float s = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const unsigned si = __float_as_uint(s);
-    const u32x2 c = __builtin_amdgcn_permlane32_swap(si, si, false, false);
-    return __uint_as_float(c[0]) + __uint_as_float(c[1]);
-}
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: K steps of
 // the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
@@ -176,18 +128,14 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             for (int ks = 0; ks < KSH; ++ks)
                 wh[h][ob][ks] = lds[LY::WHA + ((h * NB + ob) * KSH + ks) * 64 + lane];
 
-    // ---- per-lane level constants for the first layer's B operand
-    // Lanes whose level 4 s + g does not exist sample level 0 instead: their
+    // ---- the level each lane samples for K step s of the first layer.  Lanes
+    // whose level 4 s + g does not exist sample level 0 instead: their
     // first-layer weights are zero, so the (finite) value is ignored.
-    float inv[LS];
-    int loff[LS], pitch[LS];
+    LaneLevel lv[LS];
 #pragma unroll
     for (int s = 0; s < LS; ++s) {
         const int k = 4 * s + g;
-        const int kk = k < L ? k : 0;
-        inv[s] = pow2_neg(kk);
-        loff[s] = LY::LAT + box_offset(kk);
-        pitch[s] = box_pitch(kk);
+        lane_level_init(lv[s], k < L ? k : 0, LY::LAT);
     }
 
     const int H = p.H, W = p.W;
@@ -196,51 +144,18 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     // biases in its partial sums.
     const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
-    constexpr int KS1 = KSH < 4 * NB ? KSH : 4 * NB;   // live registers of a hidden activation
+    constexpr int KS1 = KSH;   // live registers of a hidden activation
 
     for (int t = blk; t < tiles; t += blocks_per_image) {
         const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
         const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         __syncthreads();   // every wavefront is done with the previous tile's boxes
-#pragma unroll
-        for (int k = 0; k < 4 * LS; ++k) {
-            if (k < L) {
-                const float iv = pow2_neg(k);
-                const int hk = p.hk[k], wk = p.wk[k];
-                const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
-                const float *src = p.lat[k] + (int64_t)b * hk * wk;
-                float *dst = lds + LY::LAT + box_offset(k);
-                const int n = box_floats(k), pc = box_pitch(k);   // constants once unrolled
-#pragma unroll
-                for (int i0 = 0; i0 < n; i0 += kThreads) {
-                    const int i = i0 + tid;
-                    if (i0 + kThreads <= n || i < n) {
-                        const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
-                        dst[i] = src[(int64_t)r * wk + c];
-                    }
-                }
-            }
-        }
+        stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
         __syncthreads();
-
-        // Column part of every level's taps for the tile's four 16-pixel columns.
-        int coff[LS][4];
-        float clx[LS][4];
-        int rbase[LS];
 #pragma unroll
-        for (int s = 0; s < LS; ++s) {
-            const int rx = src_floor(tx0, inv[s]);
-            rbase[s] = src_floor(ty0, inv[s]);
-#pragma unroll
-            for (int cg = 0; cg < 4; ++cg) {
-                const int x = min(tx0 + 16 * cg + col, tx1);
-                const float sx = fmaxf(((float)x + 0.5f) * inv[s] - 0.5f, 0.0f);
-                const int x0 = (int)sx;
-                clx[s][cg] = sx - (float)x0;
-                coff[s][cg] = loff[s] + x0 - rx;
-            }
-        }
+        for (int s = 0; s < LS; ++s)
+            lane_level_tile(lv[s], ty0, tx0, tx1, col);
 
 #pragma unroll 1
         for (int rr = 0; rr < 2; ++rr) {
@@ -250,12 +165,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             int roff[LS];
             float rly[LS];
 #pragma unroll
-            for (int s = 0; s < LS; ++s) {
-                const float sy = fmaxf(((float)y + 0.5f) * inv[s] - 0.5f, 0.0f);
-                const int y0 = (int)sy;
-                rly[s] = sy - (float)y0;
-                roff[s] = (y0 - rbase[s]) * pitch[s];
-            }
+            for (int s = 0; s < LS; ++s)
+                lane_level_row(lv[s], y, roff[s], rly[s]);
             const int64_t orow = obase + (int64_t)y * W + tx0 + col;
 
 #pragma unroll
@@ -270,13 +181,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                     d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + (ob * 64 + lane) * 4]);
 #pragma unroll
                 for (int s = 0; s < LS; ++s) {
-                    const float *q0 = lds + roff[s] + coff[s][cg];
-                    const float *q1 = q0 + pitch[s];
-                    const float a = q0[0], bq = q0[1], c = q1[0], e = q1[1];
-                    const float lx = clx[s][cg];
-                    const float top = __builtin_fmaf(lx, bq - a, a);
-                    const float bot = __builtin_fmaf(lx, e - c, c);
-                    const float u = __builtin_fmaf(rly[s], bot - top, top);
+                    const float u = lane_level_sample(lds, lv[s], roff[s], rly[s], cg);
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
                         d[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[ob][s], u, d[ob], 0, 0, 0);
@@ -318,19 +223,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                 o1 = row_sum(o1);
                 o2 = row_sum(o2);
 
-                if (g < 3 && tx0 + 16 * cg + col <= tx1) {
-                    const float v = g == 0 ? o0 : (g == 1 ? o1 : o2);
-                    const int64_t o = orow + 16 * cg;
-                    if (p.out_kind == OUT_RAW_F32) {
-                        static_cast<float *>(p.out)[o] = v;
-                    } else {
-                        const float cl = fminf(fmaxf(v, 0.0f), 1.0f);
-                        if (p.out_kind == OUT_CLAMPED_F32)
-                            static_cast<float *>(p.out)[o] = cl;
-                        else
-                            static_cast<uint8_t *>(p.out)[o] = (uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f));
-                    }
-                }
+                if (g < 3 && tx0 + 16 * cg + col <= tx1)
+                    store_out(p, orow + 16 * cg, g == 0 ? o0 : (g == 1 ? o1 : o2));
             }
         }
     }
@@ -338,23 +232,16 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 
 int hidden_blocks(int nl, const int32_t *widths);
 
+// Hidden K steps the shape needs: ceil(width / 4) of the widest hidden input.
+int hidden_ksteps(int nl, const int32_t *widths);
+
 template <int NB, int NH, int LS, int KSH>
 hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
 {
     const int tiles_x = (p.W + TW - 1) / TW, tiles_y = (p.H + TH - 1) / TH;
     const int tiles = tiles_x * tiles_y;
-    // As many workgroups as can be resident at once, split evenly over images.
     static int occ = 0;
-    if (occ == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mfma_f32<NB, NH, LS, KSH>, kThreads, 0) != hipSuccess ||
-            n < 1)
-            n = 2;
-        occ = n;
-    }
-    const int target = occ * num_cus;
-    int bpi = (target + p.batch - 1) / p.batch;
-    bpi = bpi < 1 ? 1 : (bpi > tiles ? tiles : bpi);
+    const int bpi = blocks_per_image(k_mfma_f32<NB, NH, LS, KSH>, p, num_cus, tiles, occ);
     const int64_t nblocks = (int64_t)bpi * p.batch;
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
@@ -362,9 +249,6 @@ hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
                        tiles_x, tiles);
     return hipGetLastError();
 }
-
-// Hidden K steps the shape needs: ceil(width / 4) of the widest hidden input.
-int hidden_ksteps(int nl, const int32_t *widths);
 
 template <int NH>
 hipError_t launch_nh(const DecodeParams &p, hipStream_t s, int num_cus)

@@ -88,7 +88,7 @@ def _check_u8_band(got, ref_clamped, ref_u8, what):
     assert np.all(np.abs(diff) <= 1), what
 
 
-FULL = ["pic64", "kodak768", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k"]
+FULL = ["pic64", "kodak768", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k", "kodak768_paper"]
 F32_VARIANTS = ["valu", "mfma_f32"]
 
 
@@ -263,3 +263,56 @@ def test_run_rejects_bad_arguments_before_launch():
     assert run(h, 2, ptrs, w.data_ptr(), 20, b.data_ptr(), 7, out.data_ptr()) == D.PIC_OK
     torch.cuda.synchronize()
     dec.close()
+
+
+# ------------------------------------------------------- bf16-weight family
+
+BF16_TOL = 4e-3
+
+
+def test_workload_bf16_clamped_and_raw():
+    wl = synth.WORKLOADS["uhd4k_bf16"]
+    inp = synth.workload_inputs(wl)
+    got, info = gpu_decode(inp)                       # AUTO picks the bf16 family
+    assert info["variant"] == "mfma_bf16"
+    raw, _ = gpu_decode(inp, variant="mfma_bf16", clamp=False)
+    for rows in _strips(wl.height):
+        ref = oracle.decode_inputs(inp, out="clamped", rows=rows)
+        err = np.max(np.abs(got[:, :, rows[0]:rows[1]] - ref))
+        print(f"PARITY uhd4k_bf16 mfma_bf16 clamped rows{rows}: max err {err:.3e}", flush=True)
+        assert err <= BF16_TOL
+        refr = oracle.decode_inputs(inp, out="raw", rows=rows)
+        errr = np.max(np.abs(raw[:, :, rows[0]:rows[1]] - refr) / np.maximum(1.0, np.abs(refr)))
+        print(f"PARITY uhd4k_bf16 mfma_bf16 raw rows{rows}: max err {errr:.3e}", flush=True)
+        assert errr <= BF16_TOL
+
+
+@pytest.mark.parametrize("variant", ["mfma_bf16", "mfma_f32", "valu"])
+@pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(16, 4242), ids=str)
+def test_fuzz_bf16_weights(case, variant):
+    H, W, widths, batch, seed, shared = case
+    from paper_2609_09020_amd import decoder as D
+    inp = synth.make_inputs(H, W, widths[0], widths, batch=batch, seed=seed, latent="normal",
+                            latent_scale=1.5, bias="normal", shared_weights=shared, weight_dtype="bf16")
+    nl = len(widths) - 1
+    if variant != "valu" and not (2 <= nl <= 4):
+        with pytest.raises(D.PicError) as e:
+            gpu_decode(inp, variant=variant)
+        assert e.value.status == D.PIC_E_UNSUPPORTED
+        return
+    got, _ = gpu_decode(inp, variant=variant, clamp=False, shared=shared)
+    ref = oracle.decode_inputs(inp, out="raw")     # fp64 with the same bf16 weights
+    err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
+    tol = BF16_TOL if variant == "mfma_bf16" else TOL
+    print(f"PARITY bf16-weights {case} {variant}: max err {err:.3e}", flush=True)
+    assert err <= tol
+
+
+def test_bf16_family_u8_band():
+    inp = synth.make_inputs(300, 500, 8, (8, 64, 64, 3), batch=2, seed=3, weight_dtype="bf16",
+                            latent_scale=3.0, latent_clip=64)
+    got, _ = gpu_decode(inp, variant="mfma_bf16", out_dtype="u8")
+    refc = oracle.decode_inputs(inp, out="clamped")
+    # a 4e-3 bar on c puts the 8-bit code within one step of the oracle's
+    diff = np.abs(got.astype(np.int32) - np.floor(255 * refc + 0.5).astype(np.int32))
+    assert diff.max() <= 2
