@@ -20,7 +20,8 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int TH = 8;    // tile rows (two per wavefront)
-constexpr int TW = 64;   // tile columns (four 16-pixel groups per row)
+constexpr int TWG = 4;   // 16-pixel column groups per tile row
+constexpr int TW = 16 * TWG;   // tile columns
 
 // Latent box staged per level for one tile.  A tile's pixels o0 .. o1 along
 // an axis sample source indices floor(src(o0)) .. floor(src(o1)) + 1, at most
@@ -68,6 +69,24 @@ __device__ __forceinline__ float row_sum(float x)
     return __uint_as_float(c[0]) + __uint_as_float(c[1]);
 }
 
+// Lane-group sums of three per-lane partials, transposed: lane group g (< 3)
+// receives the sum over all four lane groups of partial g.  permlane16_swap
+// exchanges the odd rows of its first operand with the even rows of its
+// second; permlane32_swap exchanges the upper half of its first operand with
+// the lower half of its second.
+//   swap16(o0, o1), add  -> rows hold [o0 01, o1 01, o0 23, o1 23] (pair sums)
+//   swap16(o2, 0), add   -> rows hold [o2 01, 0,     o2 23, 0    ]
+//   swap32(first, second), add -> rows hold [o0, o1, o2, 0] (totals)
+__device__ __forceinline__ float row_sum3(float o0, float o1, float o2)
+{
+    const u32x2 a = __builtin_amdgcn_permlane16_swap(__float_as_uint(o0), __float_as_uint(o1), false, false);
+    const float s = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const u32x2 c = __builtin_amdgcn_permlane16_swap(__float_as_uint(o2), 0u, false, false);
+    const float t = __uint_as_float(c[0]) + __uint_as_float(c[1]);
+    const u32x2 e = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(t), false, false);
+    return __uint_as_float(e[0]) + __uint_as_float(e[1]);
+}
+
 // Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
 // (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
 template <int KMAX>
@@ -94,6 +113,56 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
     }
 }
 
+// The same staging split into a load phase (into registers) and a store
+// phase, so the loads can be in flight while other prologue work waits on
+// memory.  box_regs<KMAX>() registers per thread.
+__host__ __device__ constexpr int box_regs_from(int k, int kmax)
+{
+    return k >= kmax ? 0 : (box_floats(k) + kThreads - 1) / kThreads + box_regs_from(k + 1, kmax);
+}
+template <int KMAX>
+__host__ __device__ constexpr int box_regs() { return box_regs_from(0, KMAX); }
+
+template <int KMAX>
+__device__ __forceinline__ void load_boxes(float (&v)[box_regs<KMAX>()], const DecodeParams &p, int b, int ty0,
+                                           int tx0, int tid)
+{
+    int idx = 0;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        const float iv = pow2_neg(k);
+        const int kk = k < p.L ? k : 0;   // levels past L load level 0 (never stored)
+        const int hk = p.hk[kk], wk = p.wk[kk];
+        const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
+        const float *src = p.lat[kk] + (int64_t)b * hk * wk;
+        const int n = box_floats(k), pc = box_pitch(k);
+#pragma unroll
+        for (int i0 = 0; i0 < n; i0 += kThreads) {
+            const int i = min(i0 + tid, n - 1);
+            const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
+            v[idx++] = src[(int64_t)r * wk + c];
+        }
+    }
+}
+
+template <int KMAX>
+__device__ __forceinline__ void store_boxes(float *lat, const float (&v)[box_regs<KMAX>()], const DecodeParams &p,
+                                            int tid)
+{
+    int idx = 0;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+        const int n = box_floats(k);
+#pragma unroll
+        for (int i0 = 0; i0 < n; i0 += kThreads) {
+            const int i = i0 + tid;
+            if (k < p.L && i < n)
+                lat[box_offset(k) + i] = v[idx];
+            ++idx;
+        }
+    }
+}
+
 // One lane's view of one level for the current tile: where its box starts in
 // LDS, its pitch, and the horizontal tap offsets / weights of the tile's four
 // 16-pixel column groups.
@@ -102,8 +171,8 @@ struct LaneLevel {
     int loff;         // LDS offset of the level's box (floats)
     int pitch;        // box row pitch (floats)
     int rbase;        // first source row of the box
-    int coff[4];      // loff + first-tap column - first box column, per column group
-    float clx[4];     // horizontal lerp weight, per column group
+    int coff[TWG];    // loff + first-tap column - first box column, per column group
+    float clx[TWG];   // horizontal lerp weight, per column group
 };
 
 __device__ __forceinline__ void lane_level_init(LaneLevel &lv, int k, int lat_base)
@@ -118,7 +187,7 @@ __device__ __forceinline__ void lane_level_tile(LaneLevel &lv, int ty0, int tx0,
     const int rx = src_floor(tx0, lv.inv);
     lv.rbase = src_floor(ty0, lv.inv);
 #pragma unroll
-    for (int cg = 0; cg < 4; ++cg) {
+    for (int cg = 0; cg < TWG; ++cg) {
         const int x = min(tx0 + 16 * cg + col, tx1);
         const float sx = fmaxf(((float)x + 0.5f) * lv.inv - 0.5f, 0.0f);
         const int x0 = (int)sx;

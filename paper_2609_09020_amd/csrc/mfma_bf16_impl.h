@@ -85,6 +85,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     const int64_t wbase = (int64_t)b * p.w_stride;
     const int64_t bbase = (int64_t)b * p.b_stride;
 
+    // ---- the first tile's latent loads go out first, so their latency
+    // overlaps the parameter gather below
+    float boxv[box_regs<4 * LPG>()];
+    if (blk < tiles)
+        load_boxes<4 * LPG>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
+
     // ---- stage this image's parameters into LDS in operand layouts
     {
         const int N1 = p.widths[1];
@@ -130,6 +136,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     const float b3_0 = p.biases[bbase + p.boff[NH + 1] + 0];
     const float b3_1 = p.biases[bbase + p.boff[NH + 1] + 1];
     const float b3_2 = p.biases[bbase + p.boff[NH + 1] + 2];
+    if (blk < tiles)
+        store_boxes<4 * LPG>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
     u32x4 w1[NB];
@@ -163,9 +171,11 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
         const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
         const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
-        __syncthreads();
-        stage_boxes<4 * LPG>(lds + LY::LAT, p, b, ty0, tx0, tid);
-        __syncthreads();
+        if (t != blk) {       // the first tile was staged with the parameters
+            __syncthreads();   // every wavefront is done with the previous tile's boxes
+            stage_boxes<4 * LPG>(lds + LY::LAT, p, b, ty0, tx0, tid);
+            __syncthreads();
+        }
 #pragma unroll
         for (int j = 0; j < LPG; ++j)
             lane_level_tile(lv[j], ty0, tx0, tx1, col);
@@ -183,7 +193,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             const int64_t orow = obase + (int64_t)y * W + tx0 + col;
 
 #pragma unroll
-            for (int cg = 0; cg < 4; ++cg) {
+            for (int cg = 0; cg < TWG; ++cg) {
                 if (tx0 + 16 * cg > tx1)
                     break;
 
@@ -266,12 +276,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                         o1 = __builtin_fmaf(w3[1], d[ob][r], o1);
                         o2 = __builtin_fmaf(w3[2], d[ob][r], o2);
                     }
-                o0 = row_sum(o0);
-                o1 = row_sum(o1);
-                o2 = row_sum(o2);
-
+                const float v = row_sum3(o0, o1, o2);
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
-                    store_out(p, orow + 16 * cg, g == 0 ? o0 : (g == 1 ? o1 : o2));
+                    store_out(p, orow + 16 * cg, v);
             }
         }
     }

@@ -27,9 +27,11 @@
 //   operand supplies level 4 s + g of the lane's pixel at K step s.
 //
 //   Weights are gathered once per workgroup into LDS in that operand layout
-//   (zero padded), then held in VGPRs for the workgroup's lifetime; biases
-//   (accumulator layout) and the output layer's weights are read from LDS per
-//   16-pixel group.  The output layer (3 neurons) runs on the vector ALU: each
+//   (zero padded).  The first layer's operands are then held in VGPRs; the
+//   hidden layers' are read from LDS as needed (16 bytes per lane cover four
+//   K steps), which keeps VGPR use low enough for 3-5 wavefronts per SIMD;
+//   biases (accumulator layout) and the output layer's weights are read from
+//   LDS per 16-pixel group too.  The output layer (3 neurons) runs on the vector ALU: each
 //   lane forms partial sums over the hidden values it holds and two cross-lane
 //   swaps add the four lane groups.
 //
@@ -48,8 +50,9 @@ using namespace tile;
 template <int NB, int NH, int LS, int KSH>
 struct Layout {
     static constexpr int W1A = 0;                                   // [NB][LS][64]
-    static constexpr int WHA = W1A + NB * LS * 64;                  // [NH][NB][KSH][64]
-    static constexpr int B1 = WHA + NH * NB * KSH * 64;             // [NB][64][4]
+    static constexpr int KSH4 = (KSH + 3) / 4;                      // quads of hidden K steps
+    static constexpr int WHA = W1A + NB * LS * 64;                  // [NH][NB][KSH4][64][4 steps]
+    static constexpr int B1 = WHA + NH * NB * KSH4 * 256;           // [NB][64][4]
     static constexpr int BH = B1 + NB * 64 * 4;                     // [NH][NB][64][4]
     static constexpr int W3 = BH + NH * NB * 64 * 4;                // [NB][4 r][4 g][4 c]
     static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent boxes
@@ -79,6 +82,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const int64_t wbase = (int64_t)b * p.w_stride;
     const int64_t bbase = (int64_t)b * p.b_stride;
 
+    // ---- the first tile's latent loads go out first, so their latency
+    // overlaps the parameter gather below
+    float boxv[box_regs<4 * LS>()];
+    if (blk < tiles)
+        load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
+
     // ---- stage this image's parameters into LDS in operand layouts
     {
         const int N1 = p.widths[1];
@@ -87,13 +96,15 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             const int out = 16 * ob + row_neuron(ln & 15), in = 4 * step + (ln >> 4);
             lds[LY::W1A + s] = (out < N1 && in < L) ? load_weight(p, wbase + p.woff[0] + out * L + in) : 0.0f;
         }
-        for (int s = tid; s < NH * NB * KSH * 64; s += kThreads) {   // hidden layers, A layout
-            const int ln = s & 63, ks = (s >> 6) % KSH, ob = ((s >> 6) / KSH) % NB;
-            const int h = (s >> 6) / (KSH * NB);
+        constexpr int KSH4 = LY::KSH4;
+        for (int s = tid; s < NH * NB * KSH4 * 256; s += kThreads) { // hidden layers, A layout
+            const int j = s & 3, ln = (s >> 2) & 63, q = (s >> 8) % KSH4;
+            const int ob = ((s >> 8) / KSH4) % NB, h = (s >> 8) / (KSH4 * NB);
+            const int ks = 4 * q + j;
             const int fin = p.widths[1 + h], fout = p.widths[2 + h];
             const int out = 16 * ob + row_neuron(ln & 15);
             const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
-            lds[LY::WHA + s] = (out < fout && in < fin)
+            lds[LY::WHA + s] = (ks < KSH && out < fout && in < fin)
                                    ? load_weight(p, wbase + p.woff[1 + h] + out * fin + in) : 0.0f;
         }
         for (int s = tid; s < (1 + NH) * NB * 64 * 4; s += kThreads) { // biases, accumulator layout
@@ -111,6 +122,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const float b3_0 = p.biases[bbase + p.boff[NH + 1] + 0];
     const float b3_1 = p.biases[bbase + p.boff[NH + 1] + 1];
     const float b3_2 = p.biases[bbase + p.boff[NH + 1] + 2];
+    if (blk < tiles)
+        store_boxes<4 * LS>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
     float w1[NB][LS];
@@ -119,14 +132,6 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 #pragma unroll
         for (int s = 0; s < LS; ++s)
             w1[ob][s] = lds[LY::W1A + (ob * LS + s) * 64 + lane];
-    float wh[NH > 0 ? NH : 1][NB][KSH];
-#pragma unroll
-    for (int h = 0; h < NH; ++h)
-#pragma unroll
-        for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-            for (int ks = 0; ks < KSH; ++ks)
-                wh[h][ob][ks] = lds[LY::WHA + ((h * NB + ob) * KSH + ks) * 64 + lane];
 
     // ---- the level each lane samples for K step s of the first layer.  Lanes
     // whose level 4 s + g does not exist sample level 0 instead: their
@@ -150,9 +155,11 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
         const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
-        __syncthreads();   // every wavefront is done with the previous tile's boxes
-        stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
-        __syncthreads();
+        if (t != blk) {       // the first tile was staged with the parameters
+            __syncthreads();   // every wavefront is done with the previous tile's boxes
+            stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
+            __syncthreads();
+        }
 #pragma unroll
         for (int s = 0; s < LS; ++s)
             lane_level_tile(lv[s], ty0, tx0, tx1, col);
@@ -170,7 +177,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             const int64_t orow = obase + (int64_t)y * W + tx0 + col;
 
 #pragma unroll
-            for (int cg = 0; cg < 4; ++cg) {
+            for (int cg = 0; cg < TWG; ++cg) {
                 if (tx0 + 16 * cg > tx1)
                     break;   // wave-uniform: the column group lies right of the image
 
@@ -197,12 +204,25 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
                         e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BH + ((h * NB + ob) * 64 + lane) * 4]);
+                    // A operands of K steps 4q .. 4q+3 come from LDS, one 16-byte
+                    // read per output block; step 4q + j pairs with register j
+                    // of input block q.
 #pragma unroll
-                    for (int ks = 0; ks < KSH; ++ks)
+                    for (int q = 0; q < LY::KSH4; ++q) {
+                        f32x4 wq[NB];
 #pragma unroll
                         for (int ob = 0; ob < NB; ++ob)
-                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wh[h][ob][ks], d[ks >> 2][ks & 3], e[ob],
-                                                                         0, 0, 0);
+                            wq[ob] = *reinterpret_cast<const f32x4 *>(
+                                &lds[LY::WHA + ((h * NB + ob) * LY::KSH4 + q) * 256 + lane * 4]);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (4 * q + j < KSH) {
+#pragma unroll
+                                for (int ob = 0; ob < NB; ++ob)
+                                    e[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wq[ob][j], d[q][j], e[ob], 0, 0, 0);
+                            }
+                        }
+                    }
 #pragma unroll
                     for (int ks = 0; ks < KS1; ++ks)
                         d[ks >> 2][ks & 3] = relu(e[ks >> 2][ks & 3]);
@@ -219,12 +239,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                     o1 = __builtin_fmaf(w3[1], hv, o1);
                     o2 = __builtin_fmaf(w3[2], hv, o2);
                 }
-                o0 = row_sum(o0);
-                o1 = row_sum(o1);
-                o2 = row_sum(o2);
-
+                const float v = row_sum3(o0, o1, o2);
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
-                    store_out(p, orow + 16 * cg, g == 0 ? o0 : (g == 1 ? o1 : o2));
+                    store_out(p, orow + 16 * cg, v);
             }
         }
     }
