@@ -100,6 +100,54 @@ def cpu_baseline(wl, inp, target_s=12.0):
                       f"fp64 C oracle (OpenMP over rows), {dt:.1f} s"}
 
 
+def time_calls(run, K, W, stream):
+    """Average device time per call over K back-to-back calls (HIP events on
+    the launch stream) and the wall time of the K calls."""
+    import torch
+    for _ in range(W):
+        run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(K):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / K, time.perf_counter() - t0
+
+
+def width_sweep(args):
+    """Decode speed against synthesis width for the paper's net shape: L = 8
+    levels, three hidden layers of width W, 3 outputs, 768x512 (the Kodak image
+    size), fp32.  Width 8 runs in 16-wide matrix blocks (zero padded)."""
+    import torch
+    from paper_2609_09020_amd import synth
+    from paper_2609_09020_amd import decoder as D
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    H, W = 512, 768
+    for width in (8, 16, 24, 32, 40, 48, 64):
+        widths = (8, width, width, width, 3)
+        inp = synth.make_inputs(H, W, 8, widths, batch=1, seed=0, latent="laplace_int",
+                                latent_scale=2.0, latent_clip=32)
+        lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
+        wt = torch.from_numpy(inp.weights).to(dev)
+        bt = torch.from_numpy(inp.biases).to(dev)
+        for variant in ("mfma_f32", "valu"):
+            dec = D.Decoder(H, W, widths, max_batch=1, variant=variant)
+            out = dec.alloc_out(1, dev)
+            ms, wall = time_calls(lambda: dec.run(lat, wt, bt, out=out), args.steps, args.warmup, stream)
+            fpp = flops_per_pixel(widths)
+            print(json.dumps({"sweep": "width", "widths": list(widths), "variant": variant,
+                              "kernel_avg_ms": round(ms, 5), "mpixel_s": round(H * W / ms / 1e3, 1),
+                              "fps": round(1e3 / ms, 1), "flop_per_pixel": fpp,
+                              "fp32_frac": round(fpp * H * W / (ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4)}),
+                  flush=True)
+            dec.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,6 +159,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain device copy of known size (counter calibration)")
+    ap.add_argument("--width-sweep", action="store_true",
+                    help="instead of the benchmark line, time the paper's 4-layer net shape "
+                         "(8 -> W -> W -> W -> 3) at 768x512 for several widths W; one JSON line each")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -123,6 +174,10 @@ def main():
 
     from paper_2609_09020_amd import synth
     from paper_2609_09020_amd import decoder as D
+
+    if args.width_sweep:
+        width_sweep(args)
+        return
 
     wl = synth.WORKLOADS[args.workload]
     inp = synth.workload_inputs(wl)

@@ -161,6 +161,53 @@ PIC_API pic_status pic_decode_run(pic_decoder *dec, int32_t batch,
                                   const float *biases, int64_t biases_img_stride,
                                   void *out, void *stream);
 
+/*
+ * pic_decode_run_layers -- pic_decode_run with one parameter pointer and one
+ * per-image stride per layer, so some layers can be shared by every image
+ * and others given per image (the paper's split of g_s into a shared MLP^s
+ * and a per-image MLP^i, Sec. 3.1 and App. A).
+ *   layer_weights[l]        : device pointer to image 0's layer-l matrix,
+ *                             [widths[l+1]][widths[l]] row-major, weight_dtype
+ *   layer_weight_strides[l] : elements from image b's matrix to image b+1's
+ *                             (0: one matrix shared by the batch)
+ *   layer_biases[l]         : device pointer to image 0's layer-l bias (fp32)
+ *   layer_bias_strides[l]   : the same for biases
+ * The four arrays are host arrays of num_layers entries.  Other arguments,
+ * ownership and errors as pic_decode_run.
+ */
+PIC_API pic_status pic_decode_run_layers(pic_decoder *dec, int32_t batch, const float *const *latents,
+                                         const void *const *layer_weights, const int64_t *layer_weight_strides,
+                                         const float *const *layer_biases, const int64_t *layer_bias_strides,
+                                         void *out, void *stream);
+
+/*
+ * pic_fuse_modulation -- fold instance normalisation and channel modulation
+ * into the following linear layer (App. A).  For a layer out = W f~ + b whose
+ * input is f~ = gamma * (f - mu) / sigma + beta (per input channel c), the
+ * fused layer out = W' f + b' has
+ *     W'[o][c] = W[o][c] * gamma[c] / sigma[c]
+ *     b'[o]    = b[o] + sum_c W[o][c] * (beta[c] - gamma[c] * mu[c] / sigma[c])
+ * (App. A writes the same with w = W^T).  Computed per image, in double
+ * precision, rounded once to fp32.
+ *   in, out      : layer input / output widths, 1 .. PIC_MAX_WIDTH
+ *   batch        : images (0 enqueues nothing)
+ *   w, b         : device, image b's W at w + b*w_stride ([out][in] row-major),
+ *                  its bias at b + b*b_stride (strides 0: shared)
+ *   gamma, beta, mu, sigma : device, image b's vectors of `in` values at
+ *                  + b*stat_stride; sigma must be nonzero
+ *   w_fused      : device, [batch][out][in] fp32 (written)
+ *   b_fused      : device, [batch][out] fp32 (written)
+ *   stream       : hipStream_t (NULL: null stream); asynchronous
+ * Returns PIC_E_INVALID for bad sizes or NULL/misaligned pointers,
+ * PIC_E_NODEVICE without a HIP device, PIC_E_HIP for a failed launch.
+ * Outputs must not overlap the inputs.
+ */
+PIC_API pic_status pic_fuse_modulation(int32_t in, int32_t out, int32_t batch,
+                                       const float *w, int64_t w_stride, const float *b, int64_t b_stride,
+                                       const float *gamma, const float *beta, const float *mu,
+                                       const float *sigma, int64_t stat_stride,
+                                       float *w_fused, float *b_fused, void *stream);
+
 /* pic_decode_query -- describe the handle (variant, kernel, parameter counts).
  * Returns PIC_E_INVALID for NULL arguments or an unknown info->struct_size. */
 PIC_API pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info);

@@ -34,6 +34,8 @@ def _bind(path):
     lib.pic_oracle_upsample_f64.restype = ctypes.c_int
     lib.pic_oracle_upsample_f64.argtypes = [ctypes.c_int] * 4 + [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+    lib.pic_oracle_fuse_modulation_f64.restype = ctypes.c_int
+    lib.pic_oracle_fuse_modulation_f64.argtypes = [ctypes.c_int, ctypes.c_int] + [ctypes.c_void_p] * 8
     lib.pic_oracle_level_dim.restype = ctypes.c_int
     lib.pic_oracle_level_dim.argtypes = [ctypes.c_int, ctypes.c_int]
     return lib
@@ -127,6 +129,19 @@ class Oracle:
         del keep
         return res
 
+    def fuse_modulation(self, W, b, gamma, beta, mu, sigma):
+        """App. A fusion for one image (W [out][in]); returns (W', b') in fp64."""
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        out, fin = W.shape
+        arrs = [np.ascontiguousarray(a, dtype=np.float32) for a in (b, gamma, beta, mu, sigma)]
+        wf = np.empty((out, fin), dtype=np.float64)
+        bf = np.empty(out, dtype=np.float64)
+        rc = self._lib.pic_oracle_fuse_modulation_f64(fin, out, W.ctypes.data, *[a.ctypes.data for a in arrs],
+                                                      wf.ctypes.data, bf.ctypes.data)
+        if rc:
+            raise ValueError("oracle rejected the arguments")
+        return wf, bf
+
     def decode_inputs(self, inp, out: str = "clamped", precision: str = "f64",
                       nthreads: int = 0, batch_slice: slice = None, rows: tuple = None) -> np.ndarray:
         """decode() on a synth.Inputs bundle (optionally some images / rows)."""
@@ -165,3 +180,7 @@ def decode(*a, **kw):
 
 def decode_inputs(*a, **kw):
     return default().decode_inputs(*a, **kw)
+
+
+def fuse_modulation(*a, **kw):
+    return default().fuse_modulation(*a, **kw)

@@ -326,3 +326,31 @@ int pic_oracle_upsample_f64(int H, int W, int L, int batch,
     }
     return OR_OK;
 }
+
+/*
+ * Folding of instance normalisation and channel modulation into the next
+ * linear layer (App. A), in double precision.  The layer's input is
+ * f~[c] = gamma[c] * (f[c] - mu[c]) / sigma[c] + beta[c]; writing its
+ * output W f~ + b as a layer on the raw features f gives
+ *   W'[o][c] = W[o][c] * gamma[c] / sigma[c]
+ *   b'[o]    = b[o] + sum_c W[o][c] * beta[c] - sum_c W[o][c] * gamma[c] * mu[c] / sigma[c]
+ * (App. A's w is the transpose of W).  One image; W is [out][in].
+ */
+int pic_oracle_fuse_modulation_f64(int in, int out, const float *W, const float *b, const float *gamma,
+                                   const float *beta, const float *mu, const float *sigma,
+                                   double *w_fused, double *b_fused)
+{
+    if (in < 1 || out < 1 || !W || !b || !gamma || !beta || !mu || !sigma || !w_fused || !b_fused)
+        return OR_E_INVALID;
+    for (int o = 0; o < out; ++o) {
+        double shift = 0.0, mod = 0.0;
+        for (int c = 0; c < in; ++c) {
+            double w = W[(size_t)o * in + c];
+            w_fused[(size_t)o * in + c] = w * (double)gamma[c] / (double)sigma[c];
+            mod += w * (double)beta[c];
+            shift += w * (double)gamma[c] * (double)mu[c] / (double)sigma[c];
+        }
+        b_fused[o] = (double)b[o] + mod - shift;
+    }
+    return OR_OK;
+}

@@ -6,5 +6,6 @@ pixel to RGB.  The work runs in hand-written HIP kernels behind a C ABI
 (``include/pic_decode.h``); this package is the thin Python binding over it.
 """
 
-from .decoder import (Decoder, PicError, load_library, make_desc, pic_decode_create,  # noqa: F401
-                      pic_decode_destroy, pic_decode_query, pic_decode_run, pic_status_string)
+from .decoder import (Decoder, PicError, fuse_modulation, load_library, make_desc,  # noqa: F401
+                      pic_decode_create, pic_decode_destroy, pic_decode_query, pic_decode_run,
+                      pic_decode_run_layers, pic_fuse_modulation, pic_status_string)

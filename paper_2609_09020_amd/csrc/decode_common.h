@@ -44,12 +44,28 @@ __device__ __forceinline__ int src_floor(int o, float inv)
     return s <= 0.0f ? 0 : (int)s;
 }
 
-// Weight element idx of the image's parameter block, as fp32.
-__device__ __forceinline__ float load_weight(const DecodeParams &p, int64_t idx)
+// Image b's copy of layer l's parameters (wave-uniform pointers).
+struct LayerParams {
+    const void *w;    // [out][in], fp32 or bf16
+    const float *b;   // [out]
+    bool bf16;
+    __device__ __forceinline__ float weight(int idx) const
+    {
+        if (bf16)
+            return __uint_as_float((uint32_t) static_cast<const uint16_t *>(w)[idx] << 16);
+        return static_cast<const float *>(w)[idx];
+    }
+    __device__ __forceinline__ unsigned bits(int idx) const { return static_cast<const uint16_t *>(w)[idx]; }
+};
+
+__device__ __forceinline__ LayerParams layer_params(const DecodeParams &p, int l, int b)
 {
-    if (p.weights_bf16)
-        return __uint_as_float((uint32_t) static_cast<const uint16_t *>(p.weights)[idx] << 16);
-    return static_cast<const float *>(p.weights)[idx];
+    const int64_t esize = p.weights_bf16 ? 2 : 4;
+    LayerParams lp;
+    lp.w = static_cast<const char *>(p.wl[l]) + (int64_t)b * p.wls[l] * esize;
+    lp.b = p.bl[l] + (int64_t)b * p.bls[l];
+    lp.bf16 = p.weights_bf16 != 0;
+    return lp;
 }
 
 // max(x, 0) for a non-NaN float as one integer max: non-negative floats order

@@ -26,13 +26,15 @@ __device__ __forceinline__ float pow2_neg(int k)
     return __int_as_float((127 - k) << 23);   // 2^-k, exact for k < 127
 }
 
-__device__ __forceinline__ float load_weight(const DecodeParams &p, int64_t idx)
+// Element idx of image b's layer-l matrix, as fp32 (bf16 widened exactly).
+__device__ __forceinline__ float load_weight(const DecodeParams &p, int l, int b, int idx)
 {
+    const int64_t i = (int64_t)b * p.wls[l] + idx;
     if (p.weights_bf16) {
-        const uint16_t bits = static_cast<const uint16_t *>(p.weights)[idx];
+        const uint16_t bits = static_cast<const uint16_t *>(p.wl[l])[i];
         return __uint_as_float((uint32_t)bits << 16);
     }
-    return static_cast<const float *>(p.weights)[idx];
+    return static_cast<const float *>(p.wl[l])[i];
 }
 
 // Level k of image b sampled at output pixel (y, x).
@@ -64,14 +66,13 @@ template <int KIN, int KOUT>
 __device__ __forceinline__ void stage_layer(float *sW, float *sB, const DecodeParams &p, int b, int l)
 {
     const int fin = p.widths[l], fout = p.widths[l + 1];
-    const int64_t wbase = (int64_t)b * p.w_stride + p.woff[l];
     for (int i = threadIdx.x; i < KOUT * KIN; i += kThreads) {
         const int r = i / KIN, c = i - (i / KIN) * KIN;
-        sW[i] = (r < fout && c < fin) ? load_weight(p, wbase + (int64_t)r * fin + c) : 0.0f;
+        sW[i] = (r < fout && c < fin) ? load_weight(p, l, b, r * fin + c) : 0.0f;
     }
-    const int64_t bbase = (int64_t)b * p.b_stride + p.boff[l];
+    const float *bias = p.bl[l] + (int64_t)b * p.bls[l];
     for (int i = threadIdx.x; i < KOUT; i += kThreads)
-        sB[i] = i < fout ? p.biases[bbase + i] : 0.0f;
+        sB[i] = i < fout ? bias[i] : 0.0f;
 }
 
 // g[j] = act(sB[j] + sum_i sW[j][i] * h[i]) for j < N, canonical order.

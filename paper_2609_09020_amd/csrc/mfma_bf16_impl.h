@@ -45,11 +45,6 @@ struct Layout {
     static constexpr int SIZE = LAT + box_offset(4 * LPG);
 };
 
-__device__ __forceinline__ unsigned bf16_bits(const DecodeParams &p, int64_t idx)
-{
-    return static_cast<const uint16_t *>(p.weights)[idx];
-}
-
 // (x0, x1) -> {hi, lo}: the packed bfloat16 pairs (hi0, hi1) and (lo0, lo1),
 // low halves first.
 __device__ __forceinline__ u32x2 split_pair(float x0, float x1)
@@ -82,8 +77,6 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     const int b = blockIdx.x / blocks_per_image;
     const int blk = blockIdx.x - b * blocks_per_image;
     const int L = p.L;
-    const int64_t wbase = (int64_t)b * p.w_stride;
-    const int64_t bbase = (int64_t)b * p.b_stride;
 
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
@@ -94,6 +87,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     // ---- stage this image's parameters into LDS in operand layouts
     {
         const int N1 = p.widths[1];
+        const LayerParams l0 = layer_params(p, 0, b);
+#pragma unroll 1
         for (int s = tid; s < NB * 64 * 4; s += kThreads) {           // layer 1, A layout
             const int u = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
             const int out = 16 * ob + (ln & 15), gg = ln >> 4;
@@ -102,40 +97,52 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             for (int h = 0; h < 2; ++h) {
                 const int j = 2 * u + h, lvl = LPG * gg + j;
                 if (j < LPG && lvl < L && out < N1)
-                    w |= bf16_bits(p, wbase + p.woff[0] + out * L + lvl) << (16 * h);
+                    w |= l0.bits(out * L + lvl) << (16 * h);
             }
             ldsu[LY::W1A + s] = w;
         }
-        for (int s = tid; s < NH * NB * KS2 * 64 * 4; s += kThreads) { // hidden layers, A layout
-            const int u = s & 3, ln = (s >> 2) & 63, rest = s >> 8;
-            const int st = rest % KS2, ob = (rest / KS2) % NB, hl = rest / (KS2 * NB);
-            const int fin = p.widths[1 + hl], fout = p.widths[2 + hl];
-            const int out = 16 * ob + (ln & 15), gg = ln >> 4;
-            unsigned w = 0;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int j = 2 * u + h;
-                const int in = 16 * (2 * st + (j >> 2)) + 4 * gg + (j & 3);
-                if (out < fout && in < fin)
-                    w |= bf16_bits(p, wbase + p.woff[1 + hl] + out * fin + in) << (16 * h);
+        for (int hl = 0; hl < NH; ++hl) {                              // hidden layers, A layout
+            const int fin = p.widths[1 + hl], fout = p.widths[2 + hl];
+            const LayerParams lh = layer_params(p, 1 + hl, b);
+#pragma unroll 1
+            for (int s = tid; s < NB * KS2 * 64 * 4; s += kThreads) {
+                const int u = s & 3, ln = (s >> 2) & 63, rest = s >> 8;
+                const int st = rest % KS2, ob = rest / KS2;
+                const int out = 16 * ob + (ln & 15), gg = ln >> 4;
+                unsigned w = 0;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int j = 2 * u + h;
+                    const int in = 16 * (2 * st + (j >> 2)) + 4 * gg + (j & 3);
+                    if (out < fout && in < fin)
+                        w |= lh.bits(out * fin + in) << (16 * h);
+                }
+                ldsu[LY::WHA + hl * NB * KS2 * 256 + s] = w;
             }
-            ldsu[LY::WHA + s] = w;
         }
-        for (int s = tid; s < (1 + NH) * NB * 64 * 4; s += kThreads) { // biases, accumulator layout
-            const int r = s & 3, ln = (s >> 2) & 63, ob = (s >> 8) % NB, hl = (s >> 8) / NB;
-            const int n = 16 * ob + 4 * (ln >> 4) + r, fout = p.widths[1 + hl];
-            lds[LY::B1 + s] = n < fout ? p.biases[bbase + p.boff[hl] + n] : 0.0f;
+#pragma unroll
+        for (int hl = 0; hl <= NH; ++hl) {                             // biases, accumulator layout
+            const int fout = p.widths[1 + hl];
+            const float *bias = layer_params(p, hl, b).b;
+#pragma unroll 1
+            for (int s = tid; s < NB * 256; s += kThreads) {
+                const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
+                const int n = 16 * ob + 4 * (ln >> 4) + r;
+                lds[LY::B1 + hl * NB * 256 + s] = n < fout ? bias[n] : 0.0f;
+            }
         }
         const int NL = p.widths[NH + 1];
+        const LayerParams lo = layer_params(p, NH + 1, b);
+#pragma unroll 1
         for (int s = tid; s < NB * 64; s += kThreads) {                // output layer [ob][r][g][c]
             const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
             const int n = 16 * ob + 4 * gg + r;
-            lds[LY::W3 + s] = (c < 3 && n < NL) ? load_weight(p, wbase + p.woff[NH + 1] + c * NL + n) : 0.0f;
+            lds[LY::W3 + s] = (c < 3 && n < NL) ? lo.weight(c * NL + n) : 0.0f;
         }
     }
-    const float b3_0 = p.biases[bbase + p.boff[NH + 1] + 0];
-    const float b3_1 = p.biases[bbase + p.boff[NH + 1] + 1];
-    const float b3_2 = p.biases[bbase + p.boff[NH + 1] + 2];
+    const float *b3 = layer_params(p, NH + 1, b).b;
+    const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
     if (blk < tiles)
         store_boxes<4 * LPG>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
@@ -196,6 +203,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             for (int cg = 0; cg < TWG; ++cg) {
                 if (tx0 + 16 * cg > tx1)
                     break;
+                // Re-read the LDS operands per group rather than letting the
+                // compiler keep loop-invariant ones in VGPRs (occupancy).
+                asm volatile("" ::: "memory");
 
                 // layer 1: B operand = the lane's LPG upsampled levels, split
                 float u[4] = {0.0f, 0.0f, 0.0f, 0.0f};

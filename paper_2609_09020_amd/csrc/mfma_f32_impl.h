@@ -66,8 +66,7 @@ __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row
 // the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
 // 4 KSH and up are padding and skipped).
 template <int NB, int NH, int LS, int KSH>
-__global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int blocks_per_image,
-                                                       int tiles_x, int tiles)
+__global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
     using LY = Layout<NB, NH, LS, KSH>;
@@ -79,8 +78,6 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const int b = blockIdx.x / blocks_per_image;
     const int blk = blockIdx.x - b * blocks_per_image;
     const int L = p.L;
-    const int64_t wbase = (int64_t)b * p.w_stride;
-    const int64_t bbase = (int64_t)b * p.b_stride;
 
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
@@ -91,37 +88,50 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     // ---- stage this image's parameters into LDS in operand layouts
     {
         const int N1 = p.widths[1];
+        const LayerParams l0 = layer_params(p, 0, b);
+#pragma unroll 1
         for (int s = tid; s < NB * LS * 64; s += kThreads) {          // layer 1, A layout
             const int ln = s & 63, step = (s >> 6) % LS, ob = (s >> 6) / LS;
             const int out = 16 * ob + row_neuron(ln & 15), in = 4 * step + (ln >> 4);
-            lds[LY::W1A + s] = (out < N1 && in < L) ? load_weight(p, wbase + p.woff[0] + out * L + in) : 0.0f;
+            lds[LY::W1A + s] = (out < N1 && in < L) ? l0.weight(out * L + in) : 0.0f;
         }
         constexpr int KSH4 = LY::KSH4;
-        for (int s = tid; s < NH * NB * KSH4 * 256; s += kThreads) { // hidden layers, A layout
-            const int j = s & 3, ln = (s >> 2) & 63, q = (s >> 8) % KSH4;
-            const int ob = ((s >> 8) / KSH4) % NB, h = (s >> 8) / (KSH4 * NB);
-            const int ks = 4 * q + j;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {                                 // hidden layers, A layout
             const int fin = p.widths[1 + h], fout = p.widths[2 + h];
-            const int out = 16 * ob + row_neuron(ln & 15);
-            const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
-            lds[LY::WHA + s] = (ks < KSH && out < fout && in < fin)
-                                   ? load_weight(p, wbase + p.woff[1 + h] + out * fin + in) : 0.0f;
+            const LayerParams lh = layer_params(p, 1 + h, b);
+#pragma unroll 1
+            for (int s = tid; s < NB * KSH4 * 256; s += kThreads) {
+                const int j = s & 3, ln = (s >> 2) & 63, q = (s >> 8) % KSH4, ob = (s >> 8) / KSH4;
+                const int ks = 4 * q + j;
+                const int out = 16 * ob + row_neuron(ln & 15);
+                const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
+                lds[LY::WHA + h * NB * KSH4 * 256 + s] =
+                    (ks < KSH && out < fout && in < fin) ? lh.weight(out * fin + in) : 0.0f;
+            }
         }
-        for (int s = tid; s < (1 + NH) * NB * 64 * 4; s += kThreads) { // biases, accumulator layout
-            const int r = s & 3, ln = (s >> 2) & 63, ob = (s >> 8) % NB, h = (s >> 8) / NB;
-            const int n = 16 * ob + 4 * r + (ln >> 4), fout = p.widths[1 + h];
-            lds[LY::B1 + s] = n < fout ? p.biases[bbase + p.boff[h] + n] : 0.0f;
+#pragma unroll
+        for (int h = 0; h <= NH; ++h) {                                // biases, accumulator layout
+            const int fout = p.widths[1 + h];
+            const float *bias = layer_params(p, h, b).b;
+#pragma unroll 1
+            for (int s = tid; s < NB * 256; s += kThreads) {
+                const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
+                const int n = 16 * ob + 4 * r + (ln >> 4);
+                lds[LY::B1 + h * NB * 256 + s] = n < fout ? bias[n] : 0.0f;
+            }
         }
         const int NL = p.widths[NH + 1];
+        const LayerParams lo = layer_params(p, NH + 1, b);
+#pragma unroll 1
         for (int s = tid; s < NB * 64; s += kThreads) {                // output layer [ob][r][g][c]
             const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
             const int n = 16 * ob + 4 * r + gg;
-            lds[LY::W3 + s] = (c < 3 && n < NL) ? load_weight(p, wbase + p.woff[NH + 1] + c * NL + n) : 0.0f;
+            lds[LY::W3 + s] = (c < 3 && n < NL) ? lo.weight(c * NL + n) : 0.0f;
         }
     }
-    const float b3_0 = p.biases[bbase + p.boff[NH + 1] + 0];
-    const float b3_1 = p.biases[bbase + p.boff[NH + 1] + 1];
-    const float b3_2 = p.biases[bbase + p.boff[NH + 1] + 2];
+    const float *b3 = layer_params(p, NH + 1, b).b;
+    const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
     if (blk < tiles)
         store_boxes<4 * LS>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
@@ -180,6 +190,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             for (int cg = 0; cg < TWG; ++cg) {
                 if (tx0 + 16 * cg > tx1)
                     break;   // wave-uniform: the column group lies right of the image
+                // Re-read the LDS operands per group rather than letting the
+                // compiler keep loop-invariant ones in VGPRs (occupancy).
+                asm volatile("" ::: "memory");
 
                 // layer 1: K = levels, B operand = upsampled pyramid
                 f32x4 d[NB];

@@ -132,34 +132,20 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
     return PIC_OK;
 }
 
-pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *latents,
-                          const void *weights, int64_t weights_img_stride,
-                          const float *biases, int64_t biases_img_stride,
-                          void *out, void *stream)
+}  // extern "C"
+
+namespace {
+
+// Checks shared by both run entry points and the parts of the kernel
+// argument they have in common (latents, sizes, output).
+pic_status prepare(const pic_decoder *dec, int32_t batch, const float *const *latents, void *out,
+                   pic::DecodeParams &p)
 {
-    if (!dec)
-        return PIC_E_INVALID;
     const pic_decode_desc &d = dec->desc;
-    if (batch < 0 || batch > d.max_batch)
-        return PIC_E_INVALID;
-    if (weights_img_stride < 0 || biases_img_stride < 0)
-        return PIC_E_INVALID;
-    if (batch == 0)
-        return PIC_OK;
-    if (!latents || !weights || !biases || !out)
-        return PIC_E_INVALID;
-    const size_t walign = d.weight_dtype == PIC_BF16 ? 2 : 4;
-    if (((uintptr_t)weights % walign) || ((uintptr_t)biases % 4))
+    if (!latents || !out)
         return PIC_E_INVALID;
     if (d.out_dtype == PIC_F32 && ((uintptr_t)out % 4))
         return PIC_E_INVALID;
-    // Per-image parameter blocks must not overlap unless shared.
-    if (weights_img_stride != 0 && weights_img_stride < dec->weights_per_image)
-        return PIC_E_INVALID;
-    if (biases_img_stride != 0 && biases_img_stride < dec->biases_per_image)
-        return PIC_E_INVALID;
-
-    pic::DecodeParams p;
     memset(&p, 0, sizeof p);
     for (int k = 0; k < d.num_levels; ++k) {
         if (!latents[k] || ((uintptr_t)latents[k] % 4))
@@ -172,26 +158,19 @@ pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *l
     p.W = d.width;
     p.L = d.num_levels;
     p.nl = d.num_layers;
-    int32_t wo = 0, bo = 0;
     for (int l = 0; l <= d.num_layers; ++l)
         p.widths[l] = d.widths[l];
-    for (int l = 0; l < d.num_layers; ++l) {
-        p.woff[l] = wo;
-        p.boff[l] = bo;
-        wo += d.widths[l] * d.widths[l + 1];
-        bo += d.widths[l + 1];
-    }
-    p.weights = weights;
-    p.w_stride = weights_img_stride;
-    p.biases = biases;
-    p.b_stride = biases_img_stride;
     p.out = out;
     p.out_kind = d.out_dtype == PIC_U8 ? pic::OUT_U8
                : (d.flags & PIC_FLAG_NO_CLAMP) ? pic::OUT_RAW_F32 : pic::OUT_CLAMPED_F32;
     p.weights_bf16 = d.weight_dtype == PIC_BF16;
     p.batch = batch;
     p.groups_per_image = (int32_t)(((int64_t)d.height * d.width + 15) / 16);
+    return PIC_OK;
+}
 
+pic_status launch(pic_decoder *dec, const pic::DecodeParams &p, void *stream)
+{
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != dec->device) {
         (void)hipGetLastError();
@@ -215,6 +194,88 @@ pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *l
         dec->px_per_step = pxs;
     }
     return PIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *latents,
+                          const void *weights, int64_t weights_img_stride,
+                          const float *biases, int64_t biases_img_stride,
+                          void *out, void *stream)
+{
+    if (!dec)
+        return PIC_E_INVALID;
+    const pic_decode_desc &d = dec->desc;
+    if (batch < 0 || batch > d.max_batch)
+        return PIC_E_INVALID;
+    if (weights_img_stride < 0 || biases_img_stride < 0)
+        return PIC_E_INVALID;
+    if (batch == 0)
+        return PIC_OK;
+    if (!weights || !biases)
+        return PIC_E_INVALID;
+    const size_t esize = d.weight_dtype == PIC_BF16 ? 2 : 4;
+    if (((uintptr_t)weights % esize) || ((uintptr_t)biases % 4))
+        return PIC_E_INVALID;
+    // Per-image parameter blocks must not overlap unless shared.
+    if (weights_img_stride != 0 && weights_img_stride < dec->weights_per_image)
+        return PIC_E_INVALID;
+    if (biases_img_stride != 0 && biases_img_stride < dec->biases_per_image)
+        return PIC_E_INVALID;
+    pic::DecodeParams p;
+    pic_status st = prepare(dec, batch, latents, out, p);
+    if (st != PIC_OK)
+        return st;
+    int64_t wo = 0, bo = 0;
+    for (int l = 0; l < d.num_layers; ++l) {
+        p.wl[l] = static_cast<const char *>(weights) + wo * esize;
+        p.wls[l] = weights_img_stride;
+        p.bl[l] = biases + bo;
+        p.bls[l] = biases_img_stride;
+        wo += (int64_t)d.widths[l] * d.widths[l + 1];
+        bo += d.widths[l + 1];
+    }
+    return launch(dec, p, stream);
+}
+
+pic_status pic_decode_run_layers(pic_decoder *dec, int32_t batch, const float *const *latents,
+                                 const void *const *layer_weights, const int64_t *layer_weight_strides,
+                                 const float *const *layer_biases, const int64_t *layer_bias_strides,
+                                 void *out, void *stream)
+{
+    if (!dec)
+        return PIC_E_INVALID;
+    const pic_decode_desc &d = dec->desc;
+    if (batch < 0 || batch > d.max_batch)
+        return PIC_E_INVALID;
+    if (!layer_weights || !layer_weight_strides || !layer_biases || !layer_bias_strides)
+        return PIC_E_INVALID;
+    const size_t esize = d.weight_dtype == PIC_BF16 ? 2 : 4;
+    for (int l = 0; l < d.num_layers; ++l) {
+        const int64_t nw = (int64_t)d.widths[l] * d.widths[l + 1], nb = d.widths[l + 1];
+        if (!layer_weights[l] || !layer_biases[l] || ((uintptr_t)layer_weights[l] % esize) ||
+            ((uintptr_t)layer_biases[l] % 4))
+            return PIC_E_INVALID;
+        if (layer_weight_strides[l] < 0 || layer_bias_strides[l] < 0 ||
+            (layer_weight_strides[l] != 0 && layer_weight_strides[l] < nw) ||
+            (layer_bias_strides[l] != 0 && layer_bias_strides[l] < nb))
+            return PIC_E_INVALID;
+    }
+    if (batch == 0)
+        return PIC_OK;
+    pic::DecodeParams p;
+    pic_status st = prepare(dec, batch, latents, out, p);
+    if (st != PIC_OK)
+        return st;
+    for (int l = 0; l < d.num_layers; ++l) {
+        p.wl[l] = layer_weights[l];
+        p.wls[l] = layer_weight_strides[l];
+        p.bl[l] = layer_biases[l];
+        p.bls[l] = layer_bias_strides[l];
+    }
+    return launch(dec, p, stream);
 }
 
 pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info)

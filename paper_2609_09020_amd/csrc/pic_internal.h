@@ -19,12 +19,10 @@ struct DecodeParams {
     int32_t wk[PIC_MAX_LEVELS];         // ceil(W / 2^k)
     int32_t H, W, L, nl;                // image size, levels, linear layers
     int32_t widths[PIC_MAX_LAYERS + 1];
-    int32_t woff[PIC_MAX_LAYERS];       // element offset of layer l's matrix
-    int32_t boff[PIC_MAX_LAYERS];       // element offset of layer l's bias
-    const void *weights;                // fp32 or bf16 elements
-    int64_t w_stride;                   // elements between images (0: shared)
-    const float *biases;
-    int64_t b_stride;
+    const void *wl[PIC_MAX_LAYERS];     // layer l's [out][in] matrix of image 0 (fp32 or bf16)
+    int64_t wls[PIC_MAX_LAYERS];        // elements between images' copies of layer l (0: shared)
+    const float *bl[PIC_MAX_LAYERS];    // layer l's bias of image 0
+    int64_t bls[PIC_MAX_LAYERS];        // elements between images' biases of layer l (0: shared)
     void *out;                          // [batch][3][H][W]
     int32_t out_kind;                   // OutKind
     int32_t weights_bf16;               // 1: weights are bf16 bit patterns

@@ -29,8 +29,8 @@ VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,
 VARIANT_NAMES = {v: k for k, v in VARIANTS.items()}
 
 # Every symbol include/pic_decode.h declares.
-EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_query",
-           "pic_decode_destroy", "pic_status_string")
+EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_run_layers", "pic_decode_query",
+           "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation")
 
 
 class pic_decode_desc(ctypes.Structure):
@@ -74,6 +74,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pic_decode_run.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
                                    ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_decode_run_layers.restype = ctypes.c_int
+    lib.pic_decode_run_layers.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_fuse_modulation.restype = ctypes.c_int
+    lib.pic_fuse_modulation.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.pic_decode_query.restype = ctypes.c_int
     lib.pic_decode_query.argtypes = [ctypes.c_void_p, ctypes.POINTER(pic_decode_info)]
     lib.pic_decode_destroy.restype = None
@@ -123,6 +132,55 @@ def pic_decode_run(handle: int, batch: int, latent_ptrs: Sequence[int], weights_
     return load_library().pic_decode_run(handle, batch, arr if latent_ptrs is not None else None,
                                          weights_ptr, weights_img_stride, biases_ptr,
                                          biases_img_stride, out_ptr, stream)
+
+
+def pic_decode_run_layers(handle: int, batch: int, latent_ptrs: Sequence[int], layer_weight_ptrs: Sequence[int],
+                          layer_weight_strides: Sequence[int], layer_bias_ptrs: Sequence[int],
+                          layer_bias_strides: Sequence[int], out_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call with per-layer parameter pointers and strides; returns the status."""
+    n = len(layer_weight_ptrs)
+    lat = (ctypes.c_void_p * max(1, len(latent_ptrs)))(*latent_ptrs)
+    wp = (ctypes.c_void_p * n)(*layer_weight_ptrs)
+    ws = (ctypes.c_int64 * n)(*layer_weight_strides)
+    bp = (ctypes.c_void_p * n)(*layer_bias_ptrs)
+    bs = (ctypes.c_int64 * n)(*layer_bias_strides)
+    return load_library().pic_decode_run_layers(handle, batch, lat, wp, ws, bp, bs, out_ptr, stream)
+
+
+def pic_fuse_modulation(fan_in: int, fan_out: int, batch: int, w_ptr: int, w_stride: int, b_ptr: int,
+                        b_stride: int, gamma_ptr: int, beta_ptr: int, mu_ptr: int, sigma_ptr: int,
+                        stat_stride: int, w_fused_ptr: int, b_fused_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call of the App. A fusion; returns the status."""
+    return load_library().pic_fuse_modulation(fan_in, fan_out, batch, w_ptr, w_stride, b_ptr, b_stride,
+                                              gamma_ptr, beta_ptr, mu_ptr, sigma_ptr, stat_stride,
+                                              w_fused_ptr, b_fused_ptr, stream)
+
+
+def fuse_modulation(w, b, gamma, beta, mu, sigma, stream=None):
+    """torch front end of pic_fuse_modulation: w [batch][out][in], b [batch][out],
+    gamma/beta/mu/sigma [batch][in] (fp32 device tensors; a missing batch
+    dimension means shared).  Returns (w_fused [batch][out][in], b_fused [batch][out])."""
+    import torch
+    fan_out, fan_in = w.shape[-2], w.shape[-1]
+    batch = max(t.shape[0] if t.dim() > d else 1 for t, d in
+                ((w, 2), (b, 1), (gamma, 1), (beta, 1), (mu, 1), (sigma, 1)))
+    stats = [gamma, beta, mu, sigma]
+    if len({t.dim() for t in stats}) != 1:
+        raise ValueError("gamma, beta, mu and sigma must share one layout")
+    for t in (w, b, *stats):
+        if t.dtype != torch.float32 or not t.is_contiguous() or t.device.type != "cuda":
+            raise ValueError("fuse_modulation takes contiguous float32 device tensors")
+    wf = torch.empty((batch, fan_out, fan_in), dtype=torch.float32, device=w.device)
+    bf = torch.empty((batch, fan_out), dtype=torch.float32, device=w.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(w.device).cuda_stream
+    st = pic_fuse_modulation(fan_in, fan_out, batch, w.data_ptr(), fan_in * fan_out if w.dim() == 3 else 0,
+                             b.data_ptr(), fan_out if b.dim() == 2 else 0, gamma.data_ptr(), beta.data_ptr(),
+                             mu.data_ptr(), sigma.data_ptr(), fan_in if gamma.dim() == 2 else 0,
+                             wf.data_ptr(), bf.data_ptr(), int(stream))
+    if st != PIC_OK:
+        raise PicError(st, "pic_fuse_modulation")
+    return wf, bf
 
 
 def pic_decode_query(handle: int) -> dict:
@@ -218,6 +276,37 @@ class Decoder:
                             biases.data_ptr(), bs, out.data_ptr(), int(stream))
         if st != PIC_OK:
             raise PicError(st, "pic_decode_run")
+        return out
+
+    def run_layers(self, latents, layer_weights, layer_biases, out=None, batch: Optional[int] = None,
+                   stream=None):
+        """Per-layer parameters: layer_weights[l] is [batch][out][in] (per image)
+        or [out][in] (shared by the batch); layer_biases[l] likewise."""
+        import torch
+        batch = latents[0].shape[0] if batch is None else int(batch)
+        nl = len(self.widths) - 1
+        if len(layer_weights) != nl or len(layer_biases) != nl:
+            raise ValueError(f"expected {nl} layers")
+        dev = latents[0].device
+        ws, bs = [], []
+        for l in range(nl):
+            w, b = layer_weights[l], layer_biases[l]
+            shape = (self.widths[l + 1], self.widths[l])
+            if tuple(w.shape[-2:]) != shape or not w.is_contiguous() or w.device != dev:
+                raise ValueError(f"layer {l}: weights must be [..][{shape[0]}][{shape[1]}] on {dev}")
+            if b.shape[-1] != shape[0] or not b.is_contiguous() or b.dtype != torch.float32:
+                raise ValueError(f"layer {l}: bias must be contiguous float32 [..][{shape[0]}]")
+            ws.append(0 if w.dim() == 2 else shape[0] * shape[1])
+            bs.append(0 if b.dim() == 1 else shape[0])
+        if out is None:
+            out = self.alloc_out(batch, dev)
+        if stream is None:
+            stream = torch.cuda.current_stream(dev).cuda_stream
+        st = pic_decode_run_layers(self.handle, batch, [t.data_ptr() for t in latents],
+                                   [w.data_ptr() for w in layer_weights], ws,
+                                   [b.data_ptr() for b in layer_biases], bs, out.data_ptr(), int(stream))
+        if st != PIC_OK:
+            raise PicError(st, "pic_decode_run_layers")
         return out
 
     def close(self):

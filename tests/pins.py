@@ -347,7 +347,31 @@ def check_shared_weights(orc):
     assert np.array_equal(a, c)
 
 
+def check_fuse_modulation(orc):
+    """App. A: the fused layer applied to raw features equals the layer applied
+    to the normalised and modulated features (checked on random features in
+    fp64 with numpy, an independent evaluation of the unfused definition);
+    gamma = sigma, beta = mu leaves the layer unchanged."""
+    rng = np.random.default_rng(17)
+    for fin, fout in ((7, 5), (16, 3), (40, 40), (1, 1)):
+        W = rng.normal(0, 0.5, size=(fout, fin)).astype(np.float32)
+        b = rng.normal(0, 0.5, size=fout).astype(np.float32)
+        gamma = rng.normal(1, 0.5, size=fin).astype(np.float32)
+        beta = rng.normal(0, 0.5, size=fin).astype(np.float32)
+        mu = rng.normal(0, 2, size=fin).astype(np.float32)
+        sigma = (np.abs(rng.normal(1, 0.5, size=fin)) + 0.1).astype(np.float32)
+        wf, bf = orc.fuse_modulation(W, b, gamma, beta, mu, sigma)
+        f = rng.normal(0, 3, size=(200, fin))
+        g64, b64, m64, s64 = (a.astype(np.float64) for a in (gamma, beta, mu, sigma))
+        unfused = (g64 * (f - m64) / s64 + b64) @ W.astype(np.float64).T + b.astype(np.float64)
+        fused = f @ wf.T + bf
+        np.testing.assert_allclose(fused, unfused, rtol=1e-12, atol=1e-11)
+        wf2, bf2 = orc.fuse_modulation(W, b, sigma, mu, mu, sigma)   # modulation undoes the norm
+        np.testing.assert_allclose(wf2, W.astype(np.float64), rtol=1e-15)
+        np.testing.assert_allclose(bf2, b.astype(np.float64), rtol=1e-12, atol=1e-12)
+
+
 ALL_CHECKS = [check_level_dims, check_upsample_constant, check_upsample_affine,
               check_upsample_vs_torch, check_identity_net, check_mlp_vs_torch,
               check_epilogue_closed_forms, check_exact_rational, check_f32_model,
-              check_bf16_weights, check_shared_weights]
+              check_bf16_weights, check_shared_weights, check_fuse_modulation]

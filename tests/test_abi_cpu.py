@@ -127,3 +127,19 @@ def test_null_handle_is_rejected():
     info.struct_size = ctypes.sizeof(D.pic_decode_info)
     assert lib.pic_decode_query(None, ctypes.byref(info)) == D.PIC_E_INVALID
     lib.pic_decode_destroy(None)   # accepted
+
+
+def test_fuse_modulation_argument_checks_without_device():
+    f = D.pic_fuse_modulation
+    p = 4096   # never dereferenced: every call below returns before any launch
+    assert f(0, 4, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 4, -1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 4, 1, p, 15, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID      # stride < in*out
+    assert f(4, 4, 1, p + 2, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID   # misaligned
+    assert f(4, 4, 0, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_OK              # empty batch
+    if not _gpu_present():
+        assert f(4, 4, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_NODEVICE
+
+
+def test_run_layers_null_handle():
+    assert D.pic_decode_run_layers(None, 1, [0], [0], [0], [0], [0], 0) == D.PIC_E_INVALID

@@ -316,3 +316,141 @@ def test_bf16_family_u8_band():
     # a 4e-3 bar on c puts the 8-bit code within one step of the oracle's
     diff = np.abs(got.astype(np.int32) - np.floor(255 * refc + 0.5).astype(np.int32))
     assert diff.max() <= 2
+
+
+# ------------------------------------------ per-layer parameters, App. A fusion
+
+def test_run_layers_shared_and_per_image():
+    """The paper's split: the first layers shared by the batch (stride 0), the
+    last layer per image, through pic_decode_run_layers."""
+    from paper_2609_09020_amd import Decoder, synth as sy
+    for variant, wdt in (("mfma_f32", "f32"), ("valu", "f32"), ("mfma_bf16", "bf16")):
+        widths = (8, 16, 16, 16, 3)
+        batch = 3
+        inp = sy.make_inputs(48, 80, 8, widths, batch=batch, seed=21, latent="normal", latent_scale=2.0,
+                             bias="normal", weight_dtype=wdt)
+        nl = len(widths) - 1
+        sizes = [widths[l] * widths[l + 1] for l in range(nl)]
+        offs = np.cumsum([0] + sizes)
+        boffs = np.cumsum([0] + list(widths[1:]))
+        src_w = inp.weights_bf16 if wdt == "bf16" else inp.weights
+        # shared layers take image 0's parameters; the reference repeats them
+        ref_w = src_w.copy()
+        ref_b = inp.biases.copy()
+        for l in range(nl - 1):
+            ref_w[:, offs[l]:offs[l + 1]] = src_w[0, offs[l]:offs[l + 1]]
+            ref_b[:, boffs[l]:boffs[l + 1]] = inp.biases[0, boffs[l]:boffs[l + 1]]
+        dev = "cuda"
+        lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
+        lw, lb = [], []
+        for l in range(nl):
+            blk = src_w[:, offs[l]:offs[l + 1]].reshape(batch, widths[l + 1], widths[l])
+            bb = inp.biases[:, boffs[l]:boffs[l + 1]]
+            if l < nl - 1:
+                blk, bb = blk[0], bb[0]
+            if wdt == "bf16":
+                lw.append(torch.from_numpy(np.ascontiguousarray(blk).view(np.int16)).to(dev))
+            else:
+                lw.append(torch.from_numpy(np.ascontiguousarray(blk)).to(dev))
+            lb.append(torch.from_numpy(np.ascontiguousarray(bb)).to(dev))
+        dec = Decoder(48, 80, widths, weight_dtype=wdt, clamp=False, max_batch=batch, variant=variant)
+        got = dec.run_layers(lat, lw, lb)
+        torch.cuda.synchronize()
+        dec.close()
+        if wdt == "bf16":
+            ref = oracle.decode(inp.latents, None, ref_b, widths, 48, 80, out="raw", weights_bf16=ref_w)
+        else:
+            ref = oracle.decode(inp.latents, ref_w, ref_b, widths, 48, 80, out="raw")
+        err = np.max(np.abs(got.cpu().numpy() - ref) / np.maximum(1.0, np.abs(ref)))
+        print(f"PARITY run_layers {variant}: max err {err:.3e}", flush=True)
+        assert err <= (BF16_TOL if wdt == "bf16" else TOL)
+
+
+def test_fuse_modulation_matches_oracle():
+    from paper_2609_09020_amd import fuse_modulation
+    rng = np.random.default_rng(31)
+    for fin, fout, batch, shared in ((16, 3, 4, False), (40, 40, 2, True), (64, 64, 3, False), (1, 5, 1, False)):
+        W = rng.normal(0, 0.5, size=(batch, fout, fin)).astype(np.float32)
+        b = rng.normal(0, 0.5, size=(batch, fout)).astype(np.float32)
+        g, be, mu = (rng.normal(m, s, size=(batch, fin)).astype(np.float32) for m, s in ((1, .5), (0, .5), (0, 2)))
+        sg = (np.abs(rng.normal(1, .5, size=(batch, fin))) + 0.1).astype(np.float32)
+        T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+        if shared:
+            wf, bf = fuse_modulation(T(W[0]), T(b[0]), T(g), T(be), T(mu), T(sg))
+        else:
+            wf, bf = fuse_modulation(T(W), T(b), T(g), T(be), T(mu), T(sg))
+        torch.cuda.synchronize()
+        wf, bf = wf.cpu().numpy(), bf.cpu().numpy()
+        for i in range(batch):
+            src = 0 if shared else i
+            rw, rb = oracle.fuse_modulation(W[src], b[src], g[i], be[i], mu[i], sg[i])
+            # one rounding of the fp64 value to fp32
+            assert np.max(np.abs(wf[i] - rw) / np.maximum(np.abs(rw), 1e-30)) <= 2 ** -24
+            scale = np.abs(b[src]) + np.abs(W[src]).astype(np.float64) @ (np.abs(be[i]) + np.abs(g[i] * mu[i] / sg[i]))
+            assert np.all(np.abs(bf[i] - rb) <= 2 ** -23 * scale + 1e-30)
+
+
+def test_fused_network_decodes_like_modulated_network():
+    """End to end (App. A): decoding with the fused last layer equals the oracle
+    decode whose last layer is the oracle's fusion of the same statistics."""
+    from paper_2609_09020_amd import Decoder, fuse_modulation
+    rng = np.random.default_rng(41)
+    widths = (7, 40, 40, 3)
+    H, W_, batch = 64, 96, 2
+    inp = synth.make_inputs(H, W_, 7, widths, batch=batch, seed=9, latent="normal", latent_scale=2.0,
+                            bias="normal")
+    nl = 3
+    offs = np.cumsum([0] + [widths[l] * widths[l + 1] for l in range(nl)])
+    boffs = np.cumsum([0] + list(widths[1:]))
+    W3 = inp.weights[:, offs[2]:offs[3]].reshape(batch, 3, 40)
+    b3 = inp.biases[:, boffs[2]:boffs[3]]
+    g = rng.normal(1, .3, size=(batch, 40)).astype(np.float32)
+    be = rng.normal(0, .3, size=(batch, 40)).astype(np.float32)
+    mu = rng.normal(1, .5, size=(batch, 40)).astype(np.float32)
+    sg = (np.abs(rng.normal(1, .3, size=(batch, 40))) + 0.2).astype(np.float32)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    wf, bf = fuse_modulation(T(W3), T(b3), T(g), T(be), T(mu), T(sg))
+    ref_w = inp.weights.copy()
+    ref_b = inp.biases.copy()
+    for i in range(batch):
+        rw, rb = oracle.fuse_modulation(W3[i], b3[i], g[i], be[i], mu[i], sg[i])
+        ref_w[i, offs[2]:offs[3]] = rw.astype(np.float32).ravel()
+        ref_b[i, boffs[2]:boffs[3]] = rb.astype(np.float32)
+    lat = [torch.from_numpy(a).cuda() for a in inp.latents]
+    lw = [T(inp.weights[:, offs[l]:offs[l + 1]].reshape(batch, widths[l + 1], widths[l])) for l in range(2)] + [wf]
+    lb = [T(inp.biases[:, boffs[l]:boffs[l + 1]]) for l in range(2)] + [bf]
+    dec = Decoder(H, W_, widths, clamp=False, max_batch=batch, variant="mfma_f32")
+    got = dec.run_layers(lat, lw, lb)
+    torch.cuda.synchronize()
+    dec.close()
+    ref = oracle.decode(inp.latents, ref_w, ref_b, widths, H, W_, out="raw")
+    err = np.max(np.abs(got.cpu().numpy() - ref) / np.maximum(1.0, np.abs(ref)))
+    print(f"PARITY fused network: max err {err:.3e}", flush=True)
+    assert err <= TOL
+
+
+def test_run_layers_and_fuse_reject_bad_arguments():
+    from paper_2609_09020_amd import decoder as D
+    dec = D.Decoder(8, 8, (2, 4, 3), max_batch=2)
+    lat = [torch.zeros((2, 8, 8), device="cuda"), torch.zeros((2, 4, 4), device="cuda")]
+    w0 = torch.zeros((2, 4, 2), device="cuda")
+    w1 = torch.zeros((2, 3, 4), device="cuda")
+    b0 = torch.zeros((2, 4), device="cuda")
+    b1 = torch.zeros((2, 3), device="cuda")
+    out = dec.alloc_out(2, "cuda")
+    run = D.pic_decode_run_layers
+    lp = [t.data_ptr() for t in lat]
+    good = dict(lw=[w0.data_ptr(), w1.data_ptr()], ws=[8, 12], lb=[b0.data_ptr(), b1.data_ptr()], bs=[4, 3])
+    assert run(dec.handle, 2, lp, good["lw"], good["ws"], good["lb"], good["bs"], out.data_ptr()) == D.PIC_OK
+    assert run(dec.handle, 2, lp, good["lw"], [7, 12], good["lb"], good["bs"], out.data_ptr()) == D.PIC_E_INVALID
+    assert run(dec.handle, 2, lp, good["lw"], good["ws"], good["lb"], [4, -1], out.data_ptr()) == D.PIC_E_INVALID
+    assert run(dec.handle, 2, lp, [w0.data_ptr(), 0], good["ws"], good["lb"], good["bs"], out.data_ptr()) == D.PIC_E_INVALID
+    assert run(dec.handle, 3, lp, good["lw"], good["ws"], good["lb"], good["bs"], out.data_ptr()) == D.PIC_E_INVALID
+    f = D.pic_fuse_modulation
+    p = w0.data_ptr()
+    assert f(0, 4, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 65, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 4, 1, p, 3, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 4, 1, p, 0, p, 0, p, p, p, 0, 0, p, p) == D.PIC_E_INVALID
+    torch.cuda.synchronize()
+    dec.close()

@@ -40,6 +40,9 @@ MUTANTS = [
     ("f32_model_no_bias", "float acc = bias[bo + j];", "float acc = 0.0f;"),
     ("f32_model_transposed", "long idx = wo + (long)j * fin + i;\n                        float wv",
      "long idx = wo + (long)i * fout + j;\n                        float wv"),
+    ("fuse_drops_beta", "mod += w * (double)beta[c];", ""),
+    ("fuse_sigma_multiplies", "w_fused[(size_t)o * in + c] = w * (double)gamma[c] / (double)sigma[c];",
+     "w_fused[(size_t)o * in + c] = w * (double)gamma[c] * (double)sigma[c];"),
     ("f32_model_u8_truncates", "(uint8_t)floorf(fmaf(cl, 255.0f, 0.5f))", "(uint8_t)floorf(cl * 255.0f)"),
 ]
 
