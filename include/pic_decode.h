@@ -3,7 +3,7 @@
  * (gfx950).
  *
  * The operation (PIC: "Revisiting INR for Image Coding with Fast Encoding and
- * Sub-Millisecond Decoding", Sec. 3.1 with Eq. (1), Sec. 4.1 "Implementation
+ * Sub-Millisecond Decoding", Sec. 3.1 with Eq. (2), Sec. 4.1 "Implementation
  * Details", App. A): the decoder holds a pyramid of L single-channel latent
  * grids and the weights of the per-image synthesis MLP g_s.  Every level is
  * upsampled to the H x W image, the L upsampled values of a pixel form the
@@ -12,7 +12,7 @@
  *
  * Conventions fixed by this ABI where the paper leaves them open:
  *   - level k (k = 0 .. L-1) is the grid at scale 1/2^k, finest first; its
- *     size is ceil(H / 2^k) x ceil(W / 2^k) (Eq. (1) gives H / 2^k when 2^k
+ *     size is ceil(H / 2^k) x ceil(W / 2^k) (Eq. (2) gives H / 2^k when 2^k
  *     divides H; the paper numbers the same grids coarsest first, i = L - k);
  *     input channel c of the MLP is level k = c;
  *   - upsampling is bilinear with half-pixel sample centres and edge

@@ -2,8 +2,9 @@
 
 Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product library neither imports nor
-links it.  It wraps ``pic_oracle.c`` (plain C, fp64 and an fp32 model, see that
-file's header) with numpy marshalling; the arithmetic lives in the C file.
+links it.  It wraps ``pic_oracle.c`` (the synthesis step: plain C, fp64 and an fp32
+model) and ``zpr_oracle.c`` (latents from the ZpR symbol stream, fp64) with
+numpy marshalling; the arithmetic lives in the C files (see their headers).
 """
 from __future__ import annotations
 
@@ -38,6 +39,24 @@ def _bind(path):
     lib.pic_oracle_fuse_modulation_f64.argtypes = [ctypes.c_int, ctypes.c_int] + [ctypes.c_void_p] * 8
     lib.pic_oracle_level_dim.restype = ctypes.c_int
     lib.pic_oracle_level_dim.argtypes = [ctypes.c_int, ctypes.c_int]
+    # latent decoding from the ZpR symbol stream (zpr_oracle.c)
+    lib.pic_oracle_zigzag.restype = None
+    lib.pic_oracle_zigzag.argtypes = [ctypes.c_void_p]
+    lib.pic_oracle_zpr_blocks.restype = ctypes.c_long
+    lib.pic_oracle_zpr_blocks.argtypes = [ctypes.c_int] * 3
+    lib.pic_oracle_eob_offsets.restype = ctypes.c_long
+    lib.pic_oracle_eob_offsets.argtypes = [ctypes.c_void_p, ctypes.c_long, ctypes.c_int32,
+                                           ctypes.c_void_p, ctypes.c_long]
+    lib.pic_oracle_expand_symbols.restype = ctypes.c_int
+    lib.pic_oracle_expand_symbols.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                              ctypes.c_long, ctypes.c_void_p]
+    lib.pic_oracle_idct8x8_f64.restype = None
+    lib.pic_oracle_idct8x8_f64.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_oracle_unpatchify_f64.restype = ctypes.c_int
+    lib.pic_oracle_unpatchify_f64.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_oracle_zpr_decode_f64.restype = ctypes.c_int
+    lib.pic_oracle_zpr_decode_f64.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_long,
+                                                                    ctypes.c_int32, ctypes.c_void_p]
     return lib
 
 
@@ -142,6 +161,75 @@ class Oracle:
             raise ValueError("oracle rejected the arguments")
         return wf, bf
 
+    # ---------------------------------------------- ZpR stream -> latents
+
+    def zigzag(self) -> np.ndarray:
+        """JPEG zigzag scan: entry p is the row-major index of the p-th coefficient."""
+        zz = np.empty(64, dtype=np.int32)
+        self._lib.pic_oracle_zigzag(zz.ctypes.data)
+        return zz
+
+    def zpr_blocks(self, H: int, W: int, L: int) -> int:
+        """8x8 blocks of one image's pyramid."""
+        return int(self._lib.pic_oracle_zpr_blocks(H, W, L))
+
+    def eob_offsets(self, symbols, eob: int) -> np.ndarray:
+        """Positions of the eob markers in the stream (the copy_if step)."""
+        s = np.ascontiguousarray(symbols, dtype=np.int32)
+        n = int(self._lib.pic_oracle_eob_offsets(s.ctypes.data, s.size, int(eob), None, 0))
+        off = np.empty(max(n, 1), dtype=np.int64)
+        self._lib.pic_oracle_eob_offsets(s.ctypes.data, s.size, int(eob), off.ctypes.data, n)
+        return off[:n]
+
+    def expand_symbols(self, symbols, eob: int, offsets) -> tuple:
+        """Alg. 1 over every block the offsets delimit: (coefficients int32
+        [n_blocks][64] row-major, error flags)."""
+        s = np.ascontiguousarray(symbols, dtype=np.int32)
+        off = np.ascontiguousarray(offsets, dtype=np.int64)
+        co = np.empty((max(off.size, 1), 64), dtype=np.int32)
+        err = self._lib.pic_oracle_expand_symbols(s.ctypes.data, int(eob), off.ctypes.data, off.size,
+                                                  co.ctypes.data)
+        return co[:off.size], int(err)
+
+    def idct8x8(self, S) -> np.ndarray:
+        """Orthonormal 8x8 inverse DCT of one coefficient block (fp64 [8][8])."""
+        S = np.ascontiguousarray(S, dtype=np.float64).reshape(64)
+        f = np.empty(64, dtype=np.float64)
+        self._lib.pic_oracle_idct8x8_f64(S.ctypes.data, f.ctypes.data)
+        return f.reshape(8, 8)
+
+    def _split_levels(self, flat, H, W, L, batch):
+        out, o = [], 0
+        for k in range(L):
+            h, w = self.level_dim(H, k), self.level_dim(W, k)
+            out.append(flat[o:o + batch * h * w].reshape(batch, h, w))
+            o += batch * h * w
+        return out
+
+    def _level_total(self, H, W, L, batch):
+        return sum(batch * self.level_dim(H, k) * self.level_dim(W, k) for k in range(L))
+
+    def unpatchify(self, blocks, H: int, W: int, L: int, batch: int) -> list:
+        """Place [n_blocks][64] fp64 samples into the L grids [batch][h_k][w_k]."""
+        bl = np.ascontiguousarray(blocks, dtype=np.float64)
+        if bl.size != 64 * batch * self.zpr_blocks(H, W, L):
+            raise ValueError("block count does not match the pyramid")
+        flat = np.zeros(self._level_total(H, W, L, batch), dtype=np.float64)
+        if self._lib.pic_oracle_unpatchify_f64(H, W, L, batch, bl.ctypes.data, flat.ctypes.data):
+            raise ValueError("oracle rejected the arguments")
+        return self._split_levels(flat, H, W, L, batch)
+
+    def zpr_decode(self, symbols, eob: int, H: int, W: int, L: int, batch: int, fill=0.0) -> tuple:
+        """The whole step: (L fp64 grids [batch][h_k][w_k], error flags).
+        Grid samples no decoded block covers keep ``fill``."""
+        s = np.ascontiguousarray(symbols, dtype=np.int32)
+        flat = np.full(self._level_total(H, W, L, batch), fill, dtype=np.float64)
+        err = self._lib.pic_oracle_zpr_decode_f64(H, W, L, batch, s.ctypes.data, s.size, int(eob),
+                                                  flat.ctypes.data)
+        if err < 0:
+            raise ValueError("oracle rejected the arguments")
+        return self._split_levels(flat, H, W, L, batch), int(err)
+
     def decode_inputs(self, inp, out: str = "clamped", precision: str = "f64",
                       nthreads: int = 0, batch_slice: slice = None, rows: tuple = None) -> np.ndarray:
         """decode() on a synth.Inputs bundle (optionally some images / rows)."""
@@ -184,3 +272,7 @@ def decode_inputs(*a, **kw):
 
 def fuse_modulation(*a, **kw):
     return default().fuse_modulation(*a, **kw)
+
+
+def zpr_decode(*a, **kw):
+    return default().zpr_decode(*a, **kw)

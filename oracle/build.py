@@ -12,14 +12,17 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "pic_oracle.c")
+ZPR_SRC = os.path.join(HERE, "zpr_oracle.c")
+SRCS = (SRC, ZPR_SRC)
 LIB = os.path.join(HERE, "libpic_oracle.so")
 
 
-def build(verbose: bool = False, src: str = SRC, out: str = LIB) -> str:
-    """Compile ``src`` (default: the oracle) into the shared library ``out``."""
+def build(verbose: bool = False, srcs=SRCS, out: str = LIB) -> str:
+    """Compile the C files ``srcs`` (default: the oracle's) into the shared
+    library ``out``."""
     tmp = out + f".tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-           "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src, "-lm"]
+           "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, *srcs, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

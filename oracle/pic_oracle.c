@@ -9,9 +9,9 @@
  *
  * What is computed (PIC, Sec. 3.1 and App. A):
  *   - a pyramid of L single-channel latent grids; with level k = 0 the full
- *     resolution and level k scaled by 1/2^k (the paper's Eq. (1) indexes the
+ *     resolution and level k scaled by 1/2^k (the paper's Eq. (2) indexes the
  *     same grids coarsest-first, i = L - k), H_k = ceil(H / 2^k) and
- *     W_k = ceil(W / 2^k) (Eq. (1) states H / 2^(L-i) for divisible sizes);
+ *     W_k = ceil(W / 2^k) (Eq. (2) states H / 2^(L-i) for divisible sizes);
  *   - every level upsampled to H x W (Sec. 3.1: the pyramid is upsampled to
  *     the image resolution before synthesis; the kernel is not named there and
  *     is read as bilinear with half-pixel centres, edge replication and the

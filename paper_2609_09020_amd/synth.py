@@ -2,7 +2,7 @@
 
 This module only *draws* inputs: latent pyramids and MLP parameters with the
 shapes and value distributions of the decoder's workloads (PIC, Sec. 3.1
-Eq. (1) for the pyramid; Sec. 4.1 "Implementation Details" and App. A for the
+Eq. (2) for the pyramid; Sec. 4.1 "Implementation Details" and App. A for the
 per-image MLP).  It holds none of the decoder's arithmetic (no upsampling, no
 MLP evaluation), so both the HIP path and the CPU oracle can consume its
 output without sharing any of the method's code.
@@ -199,3 +199,107 @@ def workload_inputs(w: Workload, batch: Optional[int] = None, seed: Optional[int
                        latent=w.latent, latent_scale=w.latent_scale,
                        latent_clip=w.latent_clip, bias=w.bias,
                        weight_dtype=w.weight_dtype)
+
+
+# ------------------------------------------------------------------ ZpR streams
+#
+# Symbol streams as the entropy decoder hands them to the latent-decoding step
+# (PIC, Sec. 3.3 and Fig. 2; App. B Alg. 1).  The stream format: one code per
+# 8x8 block, blocks in the order image, level (coarsest first), patch row,
+# patch column; a block's code is a sequence of tokens, each either one
+# nonzero coefficient value (a literal) or a run code eob - 17 + r standing
+# for r zeros (r = 1 .. 16), and it ends with the marker eob.  The tokens
+# cover the block's zigzag positions from the first up to its last nonzero
+# coefficient; nothing is coded after it.
+#
+# The generator draws the run-length description directly: for each block the
+# zigzag positions that carry a nonzero value and those values.  It then
+# serialises it: the gap before each nonzero position as whole runs of 16 and
+# a remainder, the value, and finally the marker.  No coefficient block is
+# built and no transform is applied here.
+#
+# Distribution (a stand-in for quantised DCT coefficients of trained latents
+# at a few tenths of a bit per pixel):
+#   - 10 % of blocks are empty; 2 % are dense (every position nonzero with
+#     probability 0.7);
+#   - otherwise position 0 (DC) is nonzero with probability 0.9 and position
+#     p >= 1 with probability 0.55 exp(-(p - 1) / 5), about 3 AC values;
+#   - |DC| = 1 + Geometric(0.12), |AC| = 1 + Geometric(0.55) (mostly 1 or
+#     2), random sign, clipped to max_abs; eob = max_abs + 17, so the run
+#     codes are max_abs + 1 .. max_abs + 16.
+# That gives about 9 symbols per block, the empty blocks 1.
+
+
+def zpr_blocks_per_image(height: int, width: int, levels: int) -> int:
+    """8x8 patches of one image's pyramid (each level padded to whole patches)."""
+    n = 0
+    for k in range(levels):
+        h, w = level_shape(height, width, k)
+        n += (-(-h // 8)) * (-(-w // 8))
+    return n
+
+
+@dataclass
+class ZprStream:
+    """One latent-decoding call's input: the symbol stream of `batch` images."""
+
+    height: int
+    width: int
+    levels: int
+    batch: int
+    eob: int
+    symbols: np.ndarray          # int32 [n_symbols]
+    blocks: int                  # blocks in the stream (batch * per image)
+
+
+def make_zpr_stream(height: int, width: int, levels: int, batch: int = 1, seed: int = 0,
+                    max_abs: int = 60, empty_frac: float = 0.10, dense_frac: float = 0.02) -> ZprStream:
+    """Draw a seeded symbol stream for `batch` images of this pyramid shape."""
+    rng = np.random.default_rng(seed)
+    nb = batch * zpr_blocks_per_image(height, width, levels)
+    pos = np.arange(64)
+    prob = np.where(pos == 0, 0.9, 0.55 * np.exp(-(pos - 1) / 5.0))
+    kind = rng.random(nb)
+    p = np.broadcast_to(prob, (nb, 64)).copy()
+    p[kind < empty_frac] = 0.0
+    p[(kind >= empty_frac) & (kind < empty_frac + dense_frac)] = 0.7
+    mask = rng.random((nb, 64)) < p
+    mag_dc = 1 + rng.geometric(0.12, size=nb) - 1
+    mag_ac = 1 + rng.geometric(0.55, size=(nb, 64)) - 1
+    mag = np.where(pos[None, :] == 0, mag_dc[:, None], mag_ac)
+    sign = np.where(rng.random((nb, 64)) < 0.5, -1, 1)
+    val = np.clip(sign * mag, -max_abs, max_abs).astype(np.int64)
+    eob = max_abs + 17
+
+    g, q = np.nonzero(mask)                       # block, zigzag position (row-major order)
+    first = np.ones(g.size, dtype=bool)
+    first[1:] = g[1:] != g[:-1]
+    prev = np.empty(g.size, dtype=np.int64)
+    prev[first] = -1
+    prev[~first] = q[:-1][~first[1:]]
+    gap = q - prev - 1
+    n16, rem = gap // 16, gap % 16
+    ntok = n16 + (rem > 0) + 1                     # runs, then the literal
+    per_block = np.bincount(g, weights=ntok, minlength=nb).astype(np.int64) + 1
+    start = np.concatenate([[0], np.cumsum(per_block)[:-1]])
+    total = int(per_block.sum())
+    sym = np.empty(total, dtype=np.int64)
+    # offset of each nonzero's tokens inside its block
+    cum = np.cumsum(ntok) - ntok
+    block_first = np.concatenate([[0], np.cumsum(np.bincount(g, minlength=nb))[:-1]])
+    within = cum - cum[block_first[g]] if g.size else cum
+    at = start[g] + within
+    # runs of 16
+    r16 = np.repeat(at, n16) + (np.arange(n16.sum()) - np.repeat(np.cumsum(n16) - n16, n16))
+    sym[r16] = eob - 17 + 16
+    has_rem = rem > 0
+    sym[at[has_rem] + n16[has_rem]] = eob - 17 + rem[has_rem]
+    sym[at + n16 + has_rem] = val[g, q]
+    sym[start + per_block - 1] = eob
+    return ZprStream(height, width, levels, batch, eob, sym.astype(np.int32), nb)
+
+
+def workload_zpr_stream(w: Workload, batch: Optional[int] = None, seed: Optional[int] = None) -> ZprStream:
+    """The symbol stream of a named workload's pyramid shape."""
+    return make_zpr_stream(w.height, w.width, w.levels, w.batch if batch is None else batch,
+                           w.seed + 1000 if seed is None else seed)

@@ -6,9 +6,9 @@ AssertionError on a mismatch.  ``test_oracle_pins.py`` runs them on the real
 oracle; ``test_oracle_mutants.py`` runs them on deliberately broken copies of
 the oracle's C source to show that each plausible slip is caught.
 
-What pins what (PIC, Sec. 3.1 Eq. (1) for the pyramid, Sec. 4.1 and App. A
+What pins what (PIC, Sec. 3.1 Eq. (2) for the pyramid, Sec. 4.1 and App. A
 for the MLP):
-  * level sizes        -- Eq. (1)'s H / 2^k for divisible sizes, the smallest
+  * level sizes        -- Eq. (2)'s H / 2^k for divisible sizes, the smallest
                           covering grid otherwise (brute force);
   * upsample           -- torch's bilinear ``interpolate`` (half-pixel,
                           scale 2^k) in fp64, a tent-kernel formulation in exact
@@ -128,7 +128,7 @@ def _frac_decode(latents, weights, biases, widths, H, W):
 # ------------------------------------------------------------------ pins
 
 def check_level_dims(orc):
-    # Eq. (1): H / 2^k exactly when divisible.
+    # Eq. (2): H / 2^k exactly when divisible.
     for H in (256, 512, 768, 1536, 2048):
         for k in range(8):
             if H % (1 << k) == 0:
@@ -375,3 +375,8 @@ ALL_CHECKS = [check_level_dims, check_upsample_constant, check_upsample_affine,
               check_upsample_vs_torch, check_identity_net, check_mlp_vs_torch,
               check_epilogue_closed_forms, check_exact_rational, check_f32_model,
               check_bf16_weights, check_shared_weights, check_fuse_modulation]
+
+# the latent-decoding step (ZpR stream -> pyramid) has its pins in pins_zpr.py
+from tests.pins_zpr import ZPR_CHECKS  # noqa: E402
+
+ALL_CHECKS += ZPR_CHECKS

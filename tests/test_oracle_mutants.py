@@ -13,7 +13,7 @@ import oracle
 from oracle import build as obuild
 from tests import pins
 
-# (name, exact source fragment of the fp64 path, replacement)
+# (name, exact source fragment, replacement): pic_oracle.c (synthesis step)
 MUTANTS = [
     ("drop_bias", "acc += (double)bias[bo + j];", ""),
     ("transpose_weights", "long idx = wo + (long)j * fin + i;\n                        double wv",
@@ -46,6 +46,27 @@ MUTANTS = [
     ("f32_model_u8_truncates", "(uint8_t)floorf(fmaf(cl, 255.0f, 0.5f))", "(uint8_t)floorf(cl * 255.0f)"),
 ]
 
+# the same for zpr_oracle.c (latents from the ZpR symbol stream)
+ZPR_MUTANTS = [
+    ("zigzag_direction", "if (d % 2 == 1) {", "if (d % 2 == 0) {"),
+    ("run_off_by_one", "int run = s - eob + 17;", "int run = s - eob + 16;"),
+    ("run_threshold", "if (s >= eob - 16) {", "if (s >= eob - 17) {"),
+    ("block_starts_at_marker", "long begin = g == 0 ? 0 : offsets[g - 1] + 1;",
+     "long begin = g == 0 ? 0 : offsets[g - 1];"),
+    ("literal_not_zigzagged", "blk[zz[produced]] = s;", "blk[produced] = s;"),
+    ("idct_no_dc_norm", "double au = u == 0 ? sqrt(1.0 / 8.0) : 0.5;", "double au = 0.5;"),
+    ("idct_transposed", "acc += au * av * S[u * 8 + v]", "acc += au * av * S[v * 8 + u]"),
+    ("idct_cos_phase", "cos((2 * x + 1) * u * pi / 16.0)", "cos((2 * x) * u * pi / 16.0)"),
+    ("levels_finest_first", "for (int k = L - 1; k >= 0; --k) {", "for (int k = 0; k < L; ++k) {"),
+    ("patch_grid_transposed", "int y = py * 8 + r, x = px * 8 + c;", "int y = px * 8 + r, x = py * 8 + c;"),
+    ("patch_inner_transposed", "grid[(size_t)y * wk + x] = blk[r * 8 + c];",
+     "grid[(size_t)y * wk + x] = blk[c * 8 + r];"),
+    ("no_count_check", "if (m != nb || (n > 0 && symbols[n - 1] != eob))", "if (m > nb)"),
+    ("symbol_above_eob_is_a_run", "if (s > eob) {\n                err |= ZO_ERR_SYMBOL;\n                continue;\n            }",
+     ""),
+    ("no_symbol_count_limit", "if (produced > 64 || end - begin > 64)", "if (produced > 64)"),
+]
+
 
 def _caught(orc):
     for check in pins.ALL_CHECKS:
@@ -56,14 +77,18 @@ def _caught(orc):
     return None
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(name, old, new, tmp_path):
-    src = open(obuild.SRC).read()
-    assert src.count(old) == 1, f"mutation site for {name} not unique in pic_oracle.c"
+CASES = [(obuild.SRC,) + m for m in MUTANTS] + [(obuild.ZPR_SRC,) + m for m in ZPR_MUTANTS]
+
+
+@pytest.mark.parametrize("path,name,old,new", CASES, ids=[c[1] for c in CASES])
+def test_mutant_is_caught(path, name, old, new, tmp_path):
+    src = open(path).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique in {os.path.basename(path)}"
     mutated = src.replace(old, new)
-    csrc = tmp_path / "mutant.c"
+    csrc = tmp_path / os.path.basename(path)
     csrc.write_text(mutated)
+    srcs = [str(csrc) if s == path else s for s in obuild.SRCS]
     lib = str(tmp_path / f"libmutant_{name}.so")
-    obuild.build(src=str(csrc), out=lib)
+    obuild.build(srcs=srcs, out=lib)
     orc = oracle.Oracle(lib)
     assert _caught(orc) is not None, f"no pin rejects the {name} mutant"
