@@ -141,27 +141,40 @@ int pic_oracle_expand_symbols(const int32_t *symbols, int32_t eob, const long *o
     return err;
 }
 
-/* Orthonormal 8x8 inverse DCT (DCT-III), the definition:
- *   f[x][y] = sum_u sum_v a(u) a(v) S[u][v] cos((2x+1) u pi / 16) cos((2y+1) v pi / 16)
- * with a(0) = sqrt(1/8), a(u) = sqrt(2/8) = 1/2 otherwise; u indexes rows
- * (vertical frequency), v columns.  S and f are row-major. */
-void pic_oracle_idct8x8_f64(const double *S, double *f)
+/* Basis of the orthonormal 8-point DCT: C[x][u] = a(u) cos((2x+1) u pi / 16)
+ * with a(0) = sqrt(1/8) and a(u) = sqrt(2/8) = 1/2 otherwise. */
+static void idct_basis(double C[8][8])
 {
     const double pi = 3.14159265358979323846;
     for (int x = 0; x < 8; ++x) {
+        for (int u = 0; u < 8; ++u) {
+            double a = u == 0 ? sqrt(1.0 / 8.0) : 0.5;
+            C[x][u] = a * cos((2 * x + 1) * u * pi / 16.0);
+        }
+    }
+}
+
+/* Orthonormal 8x8 inverse DCT (DCT-III), the definition:
+ *   f[x][y] = sum_u sum_v C[x][u] C[y][v] S[u][v]
+ * u indexes rows (vertical frequency), v columns; S and f are row-major. */
+static void idct8x8(const double C[8][8], const double *S, double *f)
+{
+    for (int x = 0; x < 8; ++x) {
         for (int y = 0; y < 8; ++y) {
             double acc = 0.0;
-            for (int u = 0; u < 8; ++u) {
-                double au = u == 0 ? sqrt(1.0 / 8.0) : 0.5;
-                for (int v = 0; v < 8; ++v) {
-                    double av = v == 0 ? sqrt(1.0 / 8.0) : 0.5;
-                    acc += au * av * S[u * 8 + v] * cos((2 * x + 1) * u * pi / 16.0) *
-                           cos((2 * y + 1) * v * pi / 16.0);
-                }
-            }
+            for (int u = 0; u < 8; ++u)
+                for (int v = 0; v < 8; ++v)
+                    acc += C[x][u] * C[y][v] * S[u * 8 + v];
             f[x * 8 + y] = acc;
         }
     }
+}
+
+void pic_oracle_idct8x8_f64(const double *S, double *f)
+{
+    double C[8][8];
+    idct_basis(C);
+    idct8x8(C, S, f);
 }
 
 /* Offset of level k's grid in the concatenated output of `batch` images:
@@ -229,11 +242,14 @@ int pic_oracle_zpr_decode_f64(int H, int W, int L, int batch, const int32_t *sym
         err |= ZO_ERR_COUNT;
     long dec = m < nb ? m : nb;                  /* blocks the stream delimits */
     err |= pic_oracle_expand_symbols(symbols, eob, offsets, dec, coeffs);
+    double C[8][8];
+    idct_basis(C);
+#pragma omp parallel for schedule(static)
     for (long g = 0; g < dec; ++g) {
         double S[64];
         for (int i = 0; i < 64; ++i)
             S[i] = (double)coeffs[(size_t)g * 64 + i];
-        pic_oracle_idct8x8_f64(S, blocks + (size_t)g * 64);
+        idct8x8((const double(*)[8])C, S, blocks + (size_t)g * 64);
     }
     /* blocks past `dec` are absent: place only the decoded ones */
     if (dec == nb) {

@@ -1,11 +1,17 @@
-"""PIC synthesis decoder for AMD Instinct MI355X (gfx950).
+"""PIC decoder for AMD Instinct MI355X (gfx950).
 
-The decoder's per-pixel synthesis (PIC, Sec. 3.1 and App. A): upsample every
-level of a latent pyramid to full resolution and evaluate a small ReLU MLP per
-pixel to RGB.  The work runs in hand-written HIP kernels behind a C ABI
-(``include/pic_decode.h``); this package is the thin Python binding over it.
+Two steps of PIC's decoder run in hand-written HIP kernels behind a C ABI:
+  * the per-pixel synthesis (Sec. 3.1 and App. A): upsample every level of
+    the latent pyramid to full resolution and evaluate a small ReLU MLP per
+    pixel to RGB (``include/pic_decode.h``);
+  * the latent decoding before it (Sec. 3.3, App. B Alg. 1): expand the ZpR
+    symbol stream into 8x8 DCT blocks, inverse-transform them and place them
+    in the pyramid (``include/pic_zpr.h``).
+This package is the thin Python binding over them.
 """
 
-from .decoder import (Decoder, PicError, fuse_modulation, load_library, make_desc,  # noqa: F401
-                      pic_decode_create, pic_decode_destroy, pic_decode_query, pic_decode_run,
-                      pic_decode_run_layers, pic_fuse_modulation, pic_status_string)
+from .decoder import (Decoder, PicError, ZprDecoder, fuse_modulation, load_library,  # noqa: F401
+                      make_desc, make_zpr_desc, pic_decode_create, pic_decode_destroy,
+                      pic_decode_query, pic_decode_run, pic_decode_run_layers, pic_fuse_modulation,
+                      pic_status_string, pic_zpr_create, pic_zpr_decode, pic_zpr_destroy,
+                      pic_zpr_expand, pic_zpr_query)

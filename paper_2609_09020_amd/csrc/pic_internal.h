@@ -45,3 +45,37 @@ bool mfma_f32_supports(int L, int nl, const int32_t *widths);
 bool mfma_bf16_supports(int L, int nl, const int32_t *widths);
 
 }  // namespace pic
+
+// ------------------------------------------------------------------------
+// Latent decoding from the ZpR symbol stream (k_zpr.hip, pic_zpr.hip).
+namespace pic {
+
+constexpr int kZprThreads = 256;
+constexpr int kZprChunk = 256;     // symbols per workgroup (one per thread)
+
+// Kernel argument of both latent-decoding kernels.
+struct ZprParams {
+    const int32_t *sym;             // the stream
+    int64_t n;                      // symbols in it
+    int32_t eob;                    // end-of-block marker
+    int32_t nchunks;                // ceil(n / kZprChunk), at least 1
+    int32_t expected;               // blocks the stream must hold
+    int32_t blocks_per_image;
+    int32_t L;
+    int32_t *counts;                // [nchunks] scratch: marker counts, then their exclusive prefix
+    uint32_t *ticket;               // scratch: workgroups of the count kernel that have finished
+    int32_t *status;                // PIC_ZPR_ERR_* bits of the run
+    // levels in stream order, i = 0 the coarsest (level k = L - 1 - i)
+    int32_t first[PIC_MAX_LEVELS + 1];   // first block of stream level i inside an image
+    int32_t hk[PIC_MAX_LEVELS];
+    int32_t wk[PIC_MAX_LEVELS];
+    int32_t pw[PIC_MAX_LEVELS];          // patches per row
+    float *lat[PIC_MAX_LEVELS];          // [batch][hk][wk] of stream level i
+    int32_t *coeffs;                     // [expected][64] row-major (expand only)
+};
+
+// Enqueue the two kernels; `coeff_only` writes the expanded blocks to
+// p.coeffs instead of transforming and placing them.
+hipError_t launch_zpr(const ZprParams &p, bool coeff_only, hipStream_t s);
+
+}  // namespace pic

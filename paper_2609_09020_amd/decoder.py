@@ -1,10 +1,11 @@
 """Thin ctypes binding of libpic_decode.so (include/pic_decode.h).
 
-The functions ``pic_decode_create`` / ``pic_decode_run`` / ``pic_decode_query``
-/ ``pic_decode_destroy`` / ``pic_status_string`` mirror the C entry points one
-to one and only marshal arguments; every step of the decode runs in the HIP
-kernels behind them.  ``Decoder`` wraps a handle for use with torch tensors
-(torch supplies device memory and streams, nothing else).
+The ``pic_decode_*``, ``pic_zpr_*``, ``pic_fuse_modulation`` and
+``pic_status_string`` functions mirror the C entry points one to one and only
+marshal arguments; every step runs in the HIP kernels behind them.
+``Decoder`` (synthesis) and ``ZprDecoder`` (latents from the ZpR symbol
+stream) wrap handles for use with torch tensors (torch supplies device memory
+and streams, nothing else).
 
 There is no fallback: if the library is missing or fails to load, every call
 raises.
@@ -28,9 +29,12 @@ VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,
             "mfma_f32": PIC_VARIANT_MFMA_F32, "mfma_bf16": PIC_VARIANT_MFMA_BF16}
 VARIANT_NAMES = {v: k for k, v in VARIANTS.items()}
 
-# Every symbol include/pic_decode.h declares.
+# Every symbol include/pic_decode.h and include/pic_zpr.h declare.
 EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_run_layers", "pic_decode_query",
-           "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation")
+           "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation",
+           "pic_zpr_create", "pic_zpr_decode", "pic_zpr_expand", "pic_zpr_query", "pic_zpr_destroy")
+
+PIC_ZPR_ERR_COUNT, PIC_ZPR_ERR_OVERFLOW, PIC_ZPR_ERR_SYMBOL = 1, 2, 4
 
 
 class pic_decode_desc(ctypes.Structure):
@@ -48,6 +52,17 @@ class pic_decode_info(ctypes.Structure):
                 ("weights_per_image", ctypes.c_int64), ("biases_per_image", ctypes.c_int64),
                 ("device", ctypes.c_int32), ("pixels_per_wave_step", ctypes.c_int32),
                 ("kernel_name", ctypes.c_char * 64)]
+
+
+class pic_zpr_desc(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("height", ctypes.c_int32), ("width", ctypes.c_int32),
+                ("num_levels", ctypes.c_int32), ("max_batch", ctypes.c_int32)]
+
+
+class pic_zpr_info(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("device", ctypes.c_int32),
+                ("blocks_per_image", ctypes.c_int64), ("max_symbols", ctypes.c_int64),
+                ("scratch_bytes", ctypes.c_int64), ("symbols_per_chunk", ctypes.c_int32)]
 
 
 class PicError(RuntimeError):
@@ -89,6 +104,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pic_decode_destroy.argtypes = [ctypes.c_void_p]
     lib.pic_status_string.restype = ctypes.c_char_p
     lib.pic_status_string.argtypes = [ctypes.c_int]
+    lib.pic_zpr_create.restype = ctypes.c_int
+    lib.pic_zpr_create.argtypes = [ctypes.POINTER(pic_zpr_desc), ctypes.POINTER(ctypes.c_void_p)]
+    for name in ("pic_zpr_decode", "pic_zpr_expand"):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_zpr_query.restype = ctypes.c_int
+    lib.pic_zpr_query.argtypes = [ctypes.c_void_p, ctypes.POINTER(pic_zpr_info)]
+    lib.pic_zpr_destroy.restype = None
+    lib.pic_zpr_destroy.argtypes = [ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -197,6 +223,52 @@ def pic_decode_query(handle: int) -> dict:
 
 def pic_decode_destroy(handle: int) -> None:
     load_library().pic_decode_destroy(handle)
+
+
+def make_zpr_desc(height: int, width: int, levels: int, max_batch: int = 1) -> pic_zpr_desc:
+    d = pic_zpr_desc()
+    d.struct_size = ctypes.sizeof(pic_zpr_desc)
+    d.height, d.width, d.num_levels, d.max_batch = int(height), int(width), int(levels), int(max_batch)
+    return d
+
+
+def pic_zpr_create(desc: pic_zpr_desc) -> int:
+    """Returns the handle (an integer address); raises PicError."""
+    h = ctypes.c_void_p()
+    st = load_library().pic_zpr_create(ctypes.byref(desc), ctypes.byref(h))
+    if st != PIC_OK:
+        raise PicError(st, "pic_zpr_create")
+    return h.value
+
+
+def pic_zpr_decode(handle: int, batch: int, symbols_ptr: int, n_symbols: int, eob: int,
+                   latent_ptrs: Optional[Sequence[int]], status_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call; returns the status (no raise, for argument tests).
+    ``latent_ptrs`` is indexed by level k (finest first), as in the header."""
+    arr = None if latent_ptrs is None else (ctypes.c_void_p * len(latent_ptrs))(*latent_ptrs)
+    return load_library().pic_zpr_decode(handle, int(batch), symbols_ptr, int(n_symbols), int(eob), arr,
+                                         status_ptr, stream)
+
+
+def pic_zpr_expand(handle: int, batch: int, symbols_ptr: int, n_symbols: int, eob: int, coeffs_ptr: int,
+                   status_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call; returns the status."""
+    return load_library().pic_zpr_expand(handle, int(batch), symbols_ptr, int(n_symbols), int(eob), coeffs_ptr,
+                                         status_ptr, stream)
+
+
+def pic_zpr_query(handle: int) -> dict:
+    info = pic_zpr_info()
+    info.struct_size = ctypes.sizeof(pic_zpr_info)
+    st = load_library().pic_zpr_query(handle, ctypes.byref(info))
+    if st != PIC_OK:
+        raise PicError(st, "pic_zpr_query")
+    return dict(device=info.device, blocks_per_image=info.blocks_per_image, max_symbols=info.max_symbols,
+                scratch_bytes=info.scratch_bytes, symbols_per_chunk=info.symbols_per_chunk)
+
+
+def pic_zpr_destroy(handle: int) -> None:
+    load_library().pic_zpr_destroy(handle)
 
 
 # ------------------------------------------------------------ torch layer
@@ -312,6 +384,101 @@ class Decoder:
     def close(self):
         if getattr(self, "handle", None):
             pic_decode_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+class ZprDecoder:
+    """One latent-decoding handle (include/pic_zpr.h) for a fixed pyramid shape.
+
+    ``decode`` takes the symbol stream as a contiguous int32 device tensor and
+    returns the L latent grids (fp32 [batch][ceil(H/2^k)][ceil(W/2^k)], level
+    k = 0 finest, the layout ``Decoder.run`` takes) and a one-element int32
+    status tensor (PIC_ZPR_ERR_* bits).  ``expand`` returns Alg. 1's
+    coefficient blocks instead ([batch * blocks_per_image][64] int32).  Both
+    enqueue on torch's current stream (or ``stream``) and do not synchronise.
+    """
+
+    def __init__(self, height: int, width: int, levels: int, max_batch: int = 1):
+        self.height, self.width, self.levels = int(height), int(width), int(levels)
+        self.max_batch = int(max_batch)
+        self.handle = pic_zpr_create(make_zpr_desc(height, width, levels, max_batch))
+        self.blocks_per_image = self.info()["blocks_per_image"]
+
+    def info(self) -> dict:
+        return pic_zpr_query(self.handle)
+
+    def level_shape(self, k: int):
+        f = 1 << k
+        return (-(-self.height // f), -(-self.width // f))
+
+    def _check(self, symbols, status, batch):
+        import torch
+        if symbols.dtype != torch.int32 or symbols.dim() != 1 or not symbols.is_contiguous() \
+                or symbols.device.type != "cuda":
+            raise ValueError("symbols: need a contiguous 1-D int32 device tensor")
+        dev = symbols.device
+        if status is None:
+            status = torch.empty(1, dtype=torch.int32, device=dev)
+        if status.dtype != torch.int32 or status.device != dev or not status.is_contiguous():
+            raise ValueError("status: need an int32 device tensor")
+        if not 0 <= batch <= self.max_batch:
+            raise ValueError(f"batch {batch} outside 0 .. {self.max_batch}")
+        return dev, status
+
+    def decode(self, symbols, eob: int, batch: int = 1, latents=None, status=None, stream=None):
+        import torch
+        batch = int(batch)
+        dev, status = self._check(symbols, status, batch)
+        if latents is None:
+            latents = [torch.empty((batch,) + self.level_shape(k), dtype=torch.float32, device=dev)
+                       for k in range(self.levels)]
+        if len(latents) != self.levels:
+            raise ValueError(f"expected {self.levels} latent levels")
+        for k, t in enumerate(latents):
+            if t.dtype != torch.float32 or not t.is_contiguous() or t.device != dev or \
+                    tuple(t.shape[1:]) != self.level_shape(k) or t.shape[0] < batch:
+                raise ValueError(f"level {k}: need contiguous float32 [>= {batch}][{self.level_shape(k)}]")
+        if stream is None:
+            stream = torch.cuda.current_stream(dev).cuda_stream
+        st = pic_zpr_decode(self.handle, batch, symbols.data_ptr(), symbols.numel(), eob,
+                            [t.data_ptr() for t in latents], status.data_ptr(), int(stream))
+        if st != PIC_OK:
+            raise PicError(st, "pic_zpr_decode")
+        return latents, status
+
+    def expand(self, symbols, eob: int, batch: int = 1, coeffs=None, status=None, stream=None):
+        import torch
+        batch = int(batch)
+        dev, status = self._check(symbols, status, batch)
+        nb = batch * self.blocks_per_image
+        if coeffs is None:
+            coeffs = torch.empty((nb, 64), dtype=torch.int32, device=dev)
+        if coeffs.dtype != torch.int32 or not coeffs.is_contiguous() or coeffs.device != dev or \
+                coeffs.numel() < nb * 64:
+            raise ValueError(f"coeffs: need contiguous int32 [{nb}][64] on {dev}")
+        if stream is None:
+            stream = torch.cuda.current_stream(dev).cuda_stream
+        st = pic_zpr_expand(self.handle, batch, symbols.data_ptr(), symbols.numel(), eob, coeffs.data_ptr(),
+                            status.data_ptr(), int(stream))
+        if st != PIC_OK:
+            raise PicError(st, "pic_zpr_expand")
+        return coeffs, status
+
+    def close(self):
+        if getattr(self, "handle", None):
+            pic_zpr_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -1,6 +1,7 @@
 """C ABI checks that need no GPU: the library loads, exports exactly what
-include/pic_decode.h declares, struct layouts agree with the header, and
-invalid descriptors are rejected before any device is touched."""
+include/pic_decode.h and include/pic_zpr.h declare, struct layouts agree with
+the headers, and invalid descriptors are rejected before any device is
+touched."""
 import ctypes
 import os
 import re
@@ -13,10 +14,11 @@ from paper_2609_09020_amd import decoder as D
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "pic_decode.h")
+HEADERS = [HEADER, os.path.join(ROOT, "include", "pic_zpr.h")]
 
 
 def _declared():
-    txt = open(HEADER).read()
+    txt = "".join(open(h).read() for h in HEADERS)
     return sorted(set(re.findall(r"PIC_API\s+[\w\s\*]*?\b(pic_\w+)\s*\(", txt)))
 
 
@@ -143,3 +145,68 @@ def test_fuse_modulation_argument_checks_without_device():
 
 def test_run_layers_null_handle():
     assert D.pic_decode_run_layers(None, 1, [0], [0], [0], [0], [0], 0) == D.PIC_E_INVALID
+
+
+def test_zpr_struct_layout_matches_header(tmp_path):
+    src = tmp_path / "layout_zpr.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "pic_zpr.h"\n'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(pic_zpr_desc),'
+                   ' offsetof(pic_zpr_desc, max_batch), sizeof(pic_zpr_info),'
+                   ' offsetof(pic_zpr_info, blocks_per_image), offsetof(pic_zpr_info, scratch_bytes),'
+                   ' offsetof(pic_zpr_info, symbols_per_chunk));'
+                   'printf("%d %d %d\\n", PIC_ZPR_ERR_COUNT, PIC_ZPR_ERR_OVERFLOW, PIC_ZPR_ERR_SYMBOL);'
+                   'return 0;}\n')
+    exe = tmp_path / "layout_zpr"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(D.pic_zpr_desc), D.pic_zpr_desc.max_batch.offset, ctypes.sizeof(D.pic_zpr_info),
+            D.pic_zpr_info.blocks_per_image.offset, D.pic_zpr_info.scratch_bytes.offset,
+            D.pic_zpr_info.symbols_per_chunk.offset,
+            D.PIC_ZPR_ERR_COUNT, D.PIC_ZPR_ERR_OVERFLOW, D.PIC_ZPR_ERR_SYMBOL]
+    assert got == want
+
+
+def _zpr_create_status(**raw):
+    desc = D.make_zpr_desc(64, 64, 4, 1)
+    for k, v in raw.items():
+        setattr(desc, k, v)
+    h = ctypes.c_void_p()
+    st = pkg.load_library().pic_zpr_create(ctypes.byref(desc), ctypes.byref(h))
+    if st == D.PIC_OK:
+        pkg.pic_zpr_destroy(h.value)
+    else:
+        assert h.value is None
+    return st
+
+
+@pytest.mark.parametrize("raw", [dict(height=0), dict(width=-3), dict(num_levels=0), dict(num_levels=13),
+                                 dict(max_batch=0), dict(max_batch=65536), dict(struct_size=8),
+                                 dict(height=65536, width=32768)])
+def test_zpr_invalid_descriptors(raw):
+    assert _zpr_create_status(**raw) == D.PIC_E_INVALID
+
+
+def test_zpr_unsupported_size():
+    # 4K at 65535 images: more than 2^31 blocks in one stream
+    assert _zpr_create_status(height=2160, width=3840, num_levels=8, max_batch=65535) == D.PIC_E_UNSUPPORTED
+
+
+def test_zpr_null_arguments():
+    lib = pkg.load_library()
+    assert lib.pic_zpr_create(None, None) == D.PIC_E_INVALID
+    assert D.pic_zpr_decode(None, 1, 4096, 4, 20, [4096], 4096) == D.PIC_E_INVALID
+    assert D.pic_zpr_expand(None, 1, 4096, 4, 20, 4096, 4096) == D.PIC_E_INVALID
+    info = D.pic_zpr_info()
+    info.struct_size = ctypes.sizeof(D.pic_zpr_info)
+    assert lib.pic_zpr_query(None, ctypes.byref(info)) == D.PIC_E_INVALID
+    lib.pic_zpr_destroy(None)   # accepted
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_zpr_nodevice_on_cpu_host():
+    assert _zpr_create_status() == D.PIC_E_NODEVICE
+    with pytest.raises(pkg.PicError) as e:
+        pkg.ZprDecoder(64, 64, 4)
+    assert e.value.status == D.PIC_E_NODEVICE

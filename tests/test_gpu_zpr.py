@@ -1,0 +1,312 @@
+"""GPU parity of the latent-decoding step (include/pic_zpr.h) against the CPU
+oracle (oracle/zpr_oracle.c), through the C ABI.
+
+Bars:
+  * pic_zpr_expand (Alg. 1's integer output) -- bit-exact;
+  * status bits -- equal to the oracle's error flags;
+  * pic_zpr_decode (fp32 separable inverse DCT) -- per sample
+        |gpu - oracle| <= 1e-6 * sum |S| of the sample's block  (+ 1e-30)
+    The kernel forms T = S B^T (eight fp32 fused multiply-adds per value,
+    |basis| <= 1/2) and then B T (eight more), with the basis rounded to fp32.
+    Each stage adds at most 8 u_32 of its absolute sum, so the error is at most
+    about (8 + 8 + 2) * 2^-24 * (1/2 * 1/2) * sum|S| = 2.7e-7 * sum|S|.  The
+    test allows 1e-6 * sum|S|;
+  * samples and blocks a malformed stream does not delimit stay untouched.
+
+Inputs are the seeded streams of ``synth.make_zpr_stream`` (the workloads'
+pyramid shapes) and streams written by the test-side ZpR encoder of
+``tests/pins_zpr.py`` (dense blocks, long runs, literal zeros, negative
+markers).
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import paper_2609_09020_amd as pkg  # noqa: E402
+from paper_2609_09020_amd import decoder as D  # noqa: E402
+from paper_2609_09020_amd import synth  # noqa: E402
+from tests import pins_zpr  # noqa: E402
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.default()
+
+
+def _print_case(*a):
+    print("case:", *a, flush=True)
+
+
+def _gpu_expand(H, W, L, batch, symbols, eob, max_batch=None):
+    with pkg.ZprDecoder(H, W, L, max_batch or max(batch, 1)) as z:
+        sym = torch.from_numpy(np.ascontiguousarray(symbols, np.int32)).to(DEV)
+        co, st = z.expand(sym, eob, batch)
+        torch.cuda.synchronize()
+        return co.cpu().numpy(), int(st.item())
+
+
+def _gpu_decode(H, W, L, batch, symbols, eob, fill=None, max_batch=None):
+    with pkg.ZprDecoder(H, W, L, max_batch or max(batch, 1)) as z:
+        sym = torch.from_numpy(np.ascontiguousarray(symbols, np.int32)).to(DEV)
+        lat = None
+        if fill is not None:
+            lat = [torch.full((batch,) + z.level_shape(k), fill, dtype=torch.float32, device=DEV)
+                   for k in range(L)]
+        lat, st = z.decode(sym, eob, batch, latents=lat)
+        torch.cuda.synchronize()
+        return [t.cpu().numpy() for t in lat], int(st.item())
+
+
+def _oracle_expand(orc, symbols, eob, n_blocks):
+    off = orc.eob_offsets(symbols, eob)[:n_blocks]
+    return orc.expand_symbols(symbols, eob, off)
+
+
+def _block_abs_sums(orc, symbols, eob, H, W, L, batch):
+    """Per-sample sum |S| of the sample's block (for the decode tolerance)."""
+    nb = batch * orc.zpr_blocks(H, W, L)
+    co, _ = _oracle_expand(orc, symbols, eob, nb)
+    sums = np.zeros((nb, 64))
+    sums[:co.shape[0]] = np.abs(co.astype(np.float64)).sum(axis=1, keepdims=True)
+    return pins_zpr.place_blocks(sums, H, W, L, batch)
+
+
+def _check_decode(orc, H, W, L, batch, symbols, eob):
+    got, st = _gpu_decode(H, W, L, batch, symbols, eob)
+    want, err = orc.zpr_decode(symbols, eob, H, W, L, batch)
+    assert st == err
+    sums = _block_abs_sums(orc, symbols, eob, H, W, L, batch)
+    for k in range(L):
+        diff = np.abs(got[k].astype(np.float64) - want[k])
+        tol = 1e-6 * sums[k] + 1e-30
+        bad = diff > tol
+        assert not bad.any(), (f"level {k}: {bad.sum()} samples off, max diff {diff.max():.3g}, "
+                               f"max ratio {(diff / tol).max():.3g}")
+
+
+SHAPES = [("pic64", 64, 64, 4, 1), ("ragged", 37, 53, 4, 3), ("tiny", 8, 8, 1, 1), ("one_px", 1, 1, 3, 2),
+          ("kodak768", 512, 768, 7, 1), ("kodak768_L8", 512, 768, 8, 2), ("tall", 300, 17, 5, 2)]
+
+
+@pytest.mark.parametrize("name,H,W,L,batch", SHAPES, ids=[s[0] for s in SHAPES])
+def test_expand_bit_exact(orc, name, H, W, L, batch):
+    s = synth.make_zpr_stream(H, W, L, batch, seed=zlib.crc32(name.encode()) % 1000)
+    _print_case("expand", name, s.symbols.size)
+    got, st = _gpu_expand(H, W, L, batch, s.symbols, s.eob)
+    want, err = _oracle_expand(orc, s.symbols, s.eob, s.blocks)
+    assert st == 0 and err == 0
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("name,H,W,L,batch", SHAPES, ids=[s[0] for s in SHAPES])
+def test_decode_matches_oracle(orc, name, H, W, L, batch):
+    s = synth.make_zpr_stream(H, W, L, batch, seed=zlib.crc32(name.encode()) % 1000 + 1)
+    _print_case("decode", name, s.symbols.size)
+    _check_decode(orc, H, W, L, batch, s.symbols, s.eob)
+
+
+ENCODED = [  # (name, density, max_abs, split, literal-zero prob, eob offset)
+    ("dense_full", 1.0, 9, "greedy", 0.0, 0), ("dense_random", 0.9, 300, "random", 0.2, 3),
+    ("sparse_long_runs", 0.02, 5, "greedy", 0.0, 0), ("runs_random_split", 0.2, 40, "random", 0.5, 1),
+    ("empty", 0.0, 1, "greedy", 0.0, 0), ("big_values", 0.3, 2_000_000, "random", 0.0, 0),
+]
+
+
+@pytest.mark.parametrize("name,density,max_abs,split,lz,eoff", ENCODED, ids=[e[0] for e in ENCODED])
+def test_encoded_streams(orc, name, density, max_abs, split, lz, eoff):
+    H, W, L, batch = 48, 80, 4, 2
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    nb = batch * orc.zpr_blocks(H, W, L)
+    co = pins_zpr.random_blocks(rng, nb, density, max_abs)
+    eob = max_abs + 17 + eoff
+    stream = np.array([t for blk in co for t in pins_zpr.zpr_encode_block(blk, eob, rng, split, lz)], np.int32)
+    _print_case("encoded", name, stream.size)
+    got, st = _gpu_expand(H, W, L, batch, stream, eob)
+    assert st == 0 and np.array_equal(got, co)
+    _check_decode(orc, H, W, L, batch, stream, eob)
+
+
+def test_negative_marker(orc):
+    # eob = -3: run codes -19 .. -4, literals below -19
+    H, W, L = 24, 24, 2
+    rng = np.random.default_rng(1)
+    nb = orc.zpr_blocks(H, W, L)
+    co = -20 - np.abs(pins_zpr.random_blocks(rng, nb, 0.3, 50))
+    co[pins_zpr.random_blocks(rng, nb, 0.5, 1) == 0] = 0
+    eob = -3
+    stream = np.array([t for blk in co for t in pins_zpr.zpr_encode_block(blk, eob)], np.int32)
+    got, st = _gpu_expand(H, W, L, 1, stream, eob)
+    assert st == 0 and np.array_equal(got, co)
+    _check_decode(orc, H, W, L, 1, stream, eob)
+
+
+def test_marker_only_stream_spans_many_chunks(orc):
+    # every block empty: the stream is all markers (256 per chunk)
+    H, W, L = 512, 768, 7
+    nb = orc.zpr_blocks(H, W, L)
+    eob = 77
+    stream = np.full(nb, eob, np.int32)
+    got, st = _gpu_decode(H, W, L, 1, stream, eob)
+    assert st == 0
+    for g in got:
+        assert not np.any(g)
+
+
+MALFORMED = ["missing_last_marker", "extra_marker", "trailing_symbols", "symbol_above_eob",
+             "too_many_markers", "empty_stream", "block_too_long", "run_overflow", "first_block_too_long"]
+
+
+def _malformed(name, good, eob):
+    g = list(good)
+    if name == "missing_last_marker":
+        return g[:-1]
+    if name == "extra_marker":
+        return g + [eob]
+    if name == "trailing_symbols":
+        return g + [1, 2]
+    if name == "symbol_above_eob":
+        return [eob + 5] + g[:40] + [eob + 1] + g[40:]
+    if name == "too_many_markers":
+        return g + [eob] * 300
+    if name == "empty_stream":
+        return []
+    if name == "block_too_long":
+        i = len(g) // 2
+        while g[i] != eob:
+            i += 1
+        return g[:i + 1] + [3] * 70 + [eob] + g[i + 1:]
+    if name == "run_overflow":
+        i = len(g) // 3
+        while g[i] != eob:
+            i += 1
+        return g[:i + 1] + [eob - 1] * 5 + [eob] + g[i + 1:]
+    if name == "first_block_too_long":
+        return [2] * 66 + g
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("name", MALFORMED)
+def test_malformed_streams(orc, name):
+    H, W, L, batch = 64, 96, 4, 2
+    s = synth.make_zpr_stream(H, W, L, batch, seed=7)
+    stream = np.array(_malformed(name, s.symbols, s.eob), np.int32)
+    _print_case("malformed", name, stream.size)
+    fill = 1234.5
+    got, st = _gpu_decode(H, W, L, batch, stream, s.eob, fill=fill)
+    want, err = orc.zpr_decode(stream, s.eob, H, W, L, batch, fill=fill)
+    assert st == err and err != 0
+    if err & D.PIC_ZPR_ERR_OVERFLOW:
+        return   # the values of an over-long block are unspecified; the flag is the contract
+    for k in range(L):
+        assert np.allclose(got[k], want[k], rtol=0, atol=1e-3), f"level {k}"
+
+
+def test_full_size_batch_sampled(orc):
+    # the launch the benchmark times (768x512, 7 levels, 64 images), every
+    # sample compared for three images decoded by the oracle one by one
+    wl = synth.WORKLOADS["kodak768_b64"]
+    s = synth.workload_zpr_stream(wl)
+    H, W, L, batch = wl.height, wl.width, wl.levels, wl.batch
+    _print_case("full size", wl.name, s.symbols.size)
+    got, st = _gpu_decode(H, W, L, batch, s.symbols, s.eob)
+    assert st == 0
+    bpi = orc.zpr_blocks(H, W, L)
+    marks = np.flatnonzero(s.symbols == s.eob)
+    for b in (0, 37, batch - 1):
+        lo = 0 if b == 0 else marks[b * bpi - 1] + 1
+        hi = marks[(b + 1) * bpi - 1] + 1
+        sub = s.symbols[lo:hi]
+        want, err = orc.zpr_decode(sub, s.eob, H, W, L, 1)
+        sums = _block_abs_sums(orc, sub, s.eob, H, W, L, 1)
+        assert err == 0
+        for k in range(L):
+            diff = np.abs(got[k][b].astype(np.float64) - want[k][0])
+            assert (diff <= 1e-6 * sums[k][0] + 1e-30).all(), f"image {b} level {k}"
+
+
+def test_two_runs_reuse_scratch(orc):
+    # the arrival counter and prefix scratch are reused: a second, smaller run
+    H, W, L = 64, 64, 4
+    with pkg.ZprDecoder(H, W, L, 4) as z:
+        for batch, seed in ((4, 1), (1, 2), (3, 3)):
+            s = synth.make_zpr_stream(H, W, L, batch, seed=seed)
+            co, st = z.expand(torch.from_numpy(s.symbols).to(DEV), s.eob, batch)
+            torch.cuda.synchronize()
+            want, err = _oracle_expand(orc, s.symbols, s.eob, s.blocks)
+            assert int(st.item()) == 0 and np.array_equal(co.cpu().numpy(), want)
+
+
+def test_side_stream_and_batch_zero(orc):
+    H, W, L = 40, 40, 3
+    s = synth.make_zpr_stream(H, W, L, 2, seed=4)
+    with pkg.ZprDecoder(H, W, L, 2) as z:
+        sym = torch.from_numpy(s.symbols).to(DEV)
+        st = torch.full((1,), -7, dtype=torch.int32, device=DEV)
+        z.decode(sym, s.eob, 0, status=st)                     # enqueues nothing
+        torch.cuda.synchronize()
+        assert int(st.item()) == -7
+        side = torch.cuda.Stream()
+        with torch.cuda.stream(side):
+            lat, st2 = z.decode(sym, s.eob, 2)
+        side.synchronize()
+        want, err = orc.zpr_decode(s.symbols, s.eob, H, W, L, 2)
+        assert int(st2.item()) == 0
+        for k in range(L):
+            assert np.allclose(lat[k].cpu().numpy(), want[k], rtol=0, atol=1e-3)
+
+
+def test_argument_rejection():
+    with pkg.ZprDecoder(64, 64, 4, 2) as z:
+        h = z.handle
+        bpi = z.blocks_per_image
+        sym = torch.zeros(1024, dtype=torch.int32, device=DEV)
+        st = torch.zeros(4, dtype=torch.int32, device=DEV)
+        co = torch.zeros((2 * bpi + 1, 64), dtype=torch.int32, device=DEV)
+        p = sym.data_ptr()
+        ok = D.pic_zpr_expand(h, 1, p, 10, 20, co.data_ptr(), st.data_ptr())
+        torch.cuda.synchronize()
+        assert ok == D.PIC_OK
+        assert D.pic_zpr_expand(h, 3, p, 10, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID  # batch
+        assert D.pic_zpr_expand(h, 1, p, 65 * bpi + 1, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p, -1, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p, 10, -2**31, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p, 10, 20, co.data_ptr() + 4, st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p + 2, 10, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p, 10, 20, co.data_ptr(), 0) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, 0, 10, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        lat = [0] * 4
+        assert D.pic_zpr_decode(h, 1, p, 10, 20, lat, st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_decode(h, 1, p, 10, 20, None, st.data_ptr()) == D.PIC_E_INVALID
+        info = z.info()
+        assert info["blocks_per_image"] == bpi == oracle.default().zpr_blocks(64, 64, 4)
+        assert info["symbols_per_chunk"] == 256 and info["scratch_bytes"] > 0
+
+
+def test_latents_feed_the_synthesis(orc):
+    # symbols -> latents (GPU) -> image (GPU), checked step by step: the
+    # latents against the oracle's, and the image against the synthesis
+    # oracle applied to the GPU's own latents (the synthesis parity bar)
+    wl = synth.WORKLOADS["kodak768"]
+    H, W, L = wl.height, wl.width, wl.levels
+    s = synth.workload_zpr_stream(wl)
+    inp = synth.workload_inputs(wl)
+    got, st = _gpu_decode(H, W, L, 1, s.symbols, s.eob)
+    assert st == 0
+    want, _ = orc.zpr_decode(s.symbols, s.eob, H, W, L, 1)
+    sums = _block_abs_sums(orc, s.symbols, s.eob, H, W, L, 1)
+    for k in range(L):
+        assert (np.abs(got[k] - want[k]) <= 1e-6 * sums[k] + 1e-30).all()
+    lat_dev = [torch.from_numpy(g).to(DEV) for g in got]
+    with pkg.Decoder(H, W, wl.widths, clamp=False) as dec:
+        img = dec.run(lat_dev, torch.from_numpy(inp.weights).to(DEV), torch.from_numpy(inp.biases).to(DEV))
+        torch.cuda.synchronize()
+    ref = orc.decode(got, inp.weights, inp.biases, wl.widths, H, W, out="raw")
+    assert np.abs(img.cpu().numpy() - ref).max() <= 1e-5 * max(1.0, np.abs(ref).max())

@@ -54,9 +54,10 @@ ZPR_MUTANTS = [
     ("block_starts_at_marker", "long begin = g == 0 ? 0 : offsets[g - 1] + 1;",
      "long begin = g == 0 ? 0 : offsets[g - 1];"),
     ("literal_not_zigzagged", "blk[zz[produced]] = s;", "blk[produced] = s;"),
-    ("idct_no_dc_norm", "double au = u == 0 ? sqrt(1.0 / 8.0) : 0.5;", "double au = 0.5;"),
-    ("idct_transposed", "acc += au * av * S[u * 8 + v]", "acc += au * av * S[v * 8 + u]"),
+    ("idct_no_dc_norm", "double a = u == 0 ? sqrt(1.0 / 8.0) : 0.5;", "double a = 0.5;"),
+    ("idct_transposed", "acc += C[x][u] * C[y][v] * S[u * 8 + v];", "acc += C[x][u] * C[y][v] * S[v * 8 + u];"),
     ("idct_cos_phase", "cos((2 * x + 1) * u * pi / 16.0)", "cos((2 * x) * u * pi / 16.0)"),
+    ("idct_basis_transposed", "acc += C[x][u] * C[y][v] * S[u * 8 + v];", "acc += C[u][x] * C[v][y] * S[u * 8 + v];"),
     ("levels_finest_first", "for (int k = L - 1; k >= 0; --k) {", "for (int k = 0; k < L; ++k) {"),
     ("patch_grid_transposed", "int y = py * 8 + r, x = px * 8 + c;", "int y = px * 8 + r, x = py * 8 + c;"),
     ("patch_inner_transposed", "grid[(size_t)y * wk + x] = blk[r * 8 + c];",
