@@ -148,6 +148,127 @@ def width_sweep(args):
             dec.close()
 
 
+def zpr_bytes_per_call(wl, n_symbols):
+    """Compulsory HBM bytes of one latent-decoding call: the symbol stream read
+    once (4 B per symbol) and every latent sample written once (4 B)."""
+    from paper_2609_09020_amd import synth
+    lat = sum(h * w for h, w in (synth.level_shape(wl.height, wl.width, k) for k in range(wl.levels)))
+    return 4 * n_symbols + 4 * wl.batch * lat
+
+
+def zpr_cpu_baseline(wl, stream, target_s=12.0):
+    """The oracle's latent decoding of the workload's first image, repeated
+    until about target_s seconds of CPU work."""
+    import numpy as np
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    orc = oracle.default()
+    bpi = orc.zpr_blocks(wl.height, wl.width, wl.levels)
+    marks = np.flatnonzero(stream.symbols == stream.eob)
+    first = stream.symbols[:marks[bpi - 1] + 1]
+    n_img = 0
+    t0 = time.perf_counter()
+    while True:
+        orc.zpr_decode(first, stream.eob, wl.height, wl.width, wl.levels, 1)
+        n_img += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(n_img * wl.height * wl.width / dt / 1e6, 3), "unit": "Mpixel/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_img} decodes of the first image's symbol stream ({first.size} symbols, "
+                      f"{bpi} blocks) by the fp64 C oracle (OpenMP over blocks), {dt:.1f} s"}
+
+
+def zpr_bench(args, pipeline=False):
+    """Latent decoding from the ZpR symbol stream (``--zpr``), or that step
+    followed by the synthesis in one timed step (``--pipeline``)."""
+    import ctypes
+    import numpy as np
+    import torch
+    from paper_2609_09020_amd import synth
+    from paper_2609_09020_amd import decoder as D
+    wl = synth.WORKLOADS[args.workload]
+    zs = synth.workload_zpr_stream(wl)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    sym = torch.from_numpy(zs.symbols).to(dev)
+    z = D.ZprDecoder(wl.height, wl.width, wl.levels, wl.batch)
+    lat = [torch.empty((wl.batch,) + z.level_shape(k), dtype=torch.float32, device=dev)
+           for k in range(wl.levels)]
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    lib = D.load_library()
+    lat_arr = (ctypes.c_void_p * wl.levels)(*[t.data_ptr() for t in lat])
+    zargs = (ctypes.c_void_p(z.handle), ctypes.c_int32(wl.batch), ctypes.c_void_p(sym.data_ptr()),
+             ctypes.c_int64(zs.symbols.size), ctypes.c_int32(zs.eob), lat_arr,
+             ctypes.c_void_p(st.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+    calls = [(lib.pic_zpr_decode, zargs)]
+    dec = None
+    if pipeline:
+        inp = synth.workload_inputs(wl)
+        w = torch.from_numpy(inp.weights_bf16.view(np.int16) if inp.weights_bf16 is not None
+                             else inp.weights).to(dev)
+        b = torch.from_numpy(inp.biases).to(dev)
+        dec = D.Decoder(wl.height, wl.width, wl.widths, weight_dtype=wl.weight_dtype,
+                        out_dtype=args.out_dtype, max_batch=wl.batch, variant=args.variant)
+        out = dec.alloc_out(wl.batch, dev)
+        calls.append((lib.pic_decode_run,
+                      (ctypes.c_void_p(dec.handle), ctypes.c_int32(wl.batch), lat_arr,
+                       ctypes.c_void_p(w.data_ptr()), ctypes.c_int64(dec.nw), ctypes.c_void_p(b.data_ptr()),
+                       ctypes.c_int64(dec.nb), ctypes.c_void_p(out.data_ptr()),
+                       ctypes.c_void_p(stream.cuda_stream))))
+
+    def step():
+        for fn, a in calls:
+            r = fn(*a)
+            if r != D.PIC_OK:
+                raise D.PicError(r, fn.__name__)
+
+    step()
+    torch.cuda.synchronize()
+    if int(st.item()) != 0:
+        raise RuntimeError(f"latent decoding reported status {int(st.item())} on the benchmark stream")
+    ms, wall = time_calls(step, args.steps, args.warmup, stream)
+    px = wl.batch * wl.height * wl.width
+    nbytes = zpr_bytes_per_call(wl, zs.symbols.size)
+    name = "k_zpr_count + k_zpr_expand"
+    res = {
+        "metric": ("PIC decode without entropy decoding (ZpR stream -> latents -> RGB)" if pipeline
+                   else "PIC latent decoding (ZpR symbol stream -> latent pyramid)"),
+        "value": round(px * args.steps / wall / 1e6, 2), "unit": "Mpixel/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * wall / args.steps, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "fps": round(wl.batch * args.steps / wall, 1), "kernel_avg_ms": round(ms, 5),
+        "config": {"workload": f"{wl.name}: {wl.note}", "height": wl.height, "width": wl.width,
+                   "levels": wl.levels, "batch": wl.batch, "symbols": int(zs.symbols.size),
+                   "blocks": int(zs.blocks), "eob": int(zs.eob), "kernels": name,
+                   "parallelism": "single GPU"},
+    }
+    if not pipeline:
+        achieved = nbytes / (ms * 1e-3) / 1e9
+        traffic = load_traffic("k_zpr", args.workload, "latents")
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                           "bytes_per_launch": nbytes, "kernels": name}
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = zpr_cpu_baseline(wl, zs)
+    else:
+        res["config"].update({"widths": list(wl.widths), "weights": wl.weight_dtype,
+                              "out_dtype": args.out_dtype, "synthesis_kernel": dec.info()["kernel_name"]})
+    if args.copy_calib:
+        src = torch.full((256 << 20,), 7, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+    z.close()
+    if dec is not None:
+        dec.close()
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +283,11 @@ def main():
     ap.add_argument("--width-sweep", action="store_true",
                     help="instead of the benchmark line, time the paper's 4-layer net shape "
                          "(8 -> W -> W -> W -> 3) at 768x512 for several widths W; one JSON line each")
+    ap.add_argument("--zpr", action="store_true",
+                    help="instead of the synthesis, time the latent decoding from the ZpR symbol "
+                         "stream (pic_zpr_decode) on the workload's pyramid shape")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="time the latent decoding followed by the synthesis as one step")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -177,6 +303,9 @@ def main():
 
     if args.width_sweep:
         width_sweep(args)
+        return
+    if args.zpr or args.pipeline:
+        zpr_bench(args, pipeline=args.pipeline)
         return
 
     wl = synth.WORKLOADS[args.workload]

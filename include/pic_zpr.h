@@ -47,9 +47,10 @@ extern "C" {
 #endif
 
 /* Opaque handle: the pyramid shape, the device it was created on and a small
- * device scratch buffer (per-chunk marker counts and an arrival counter), so
- * runs neither allocate nor synchronise.  Runs on one handle must not
- * overlap: enqueue them on one stream, or synchronise between them. */
+ * device scratch buffer (per-chunk marker counts, 4 bytes per 256 symbols of
+ * the longest accepted stream), so runs neither allocate nor synchronise.
+ * Runs on one handle must not overlap: enqueue them on one stream, or
+ * synchronise between them. */
 typedef struct pic_zpr pic_zpr;
 
 /* Bits of the status word a run writes (0: the stream is well formed). */
@@ -77,12 +78,13 @@ typedef struct pic_zpr_info {
     int64_t max_symbols;        /* longest stream a run accepts at max_batch:
                                    min(65 * blocks_per_image * max_batch, 2^31 - 1)  */
     int64_t scratch_bytes;      /* device memory the handle holds                   */
-    int32_t symbols_per_chunk;  /* symbols one workgroup scans                       */
+    int32_t symbols_per_chunk;  /* symbols one workgroup scans on short streams (long
+                                   streams, from 2^18 symbols, use 4 times as many)  */
 } pic_zpr_info;
 
 /*
  * pic_zpr_create -- validate `desc` and build a handle on the current HIP
- * device; allocates its device scratch (hipMalloc) and clears it.
+ * device; allocates its device scratch (hipMalloc).
  * Returns PIC_OK; PIC_E_INVALID for a malformed descriptor or NULL `out`;
  * PIC_E_UNSUPPORTED when max_batch * blocks per image reaches 2^31;
  * PIC_E_NODEVICE when no gfx950 device is current; PIC_E_NOMEM when the handle

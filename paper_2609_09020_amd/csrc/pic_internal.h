@@ -51,19 +51,21 @@ bool mfma_bf16_supports(int L, int nl, const int32_t *widths);
 namespace pic {
 
 constexpr int kZprThreads = 256;
-constexpr int kZprChunk = 256;     // symbols per workgroup (one per thread)
+constexpr int kZprChunkSmall = 256;            // symbols per workgroup on short streams
+constexpr int kZprChunkLarge = 1024;           // ... on long ones
+constexpr int64_t kZprLargeFrom = 256 * 1024;  // stream length from which the large chunk is used
 
 // Kernel argument of both latent-decoding kernels.
 struct ZprParams {
     const int32_t *sym;             // the stream
     int64_t n;                      // symbols in it
     int32_t eob;                    // end-of-block marker
-    int32_t nchunks;                // ceil(n / kZprChunk), at least 1
+    int32_t chunk;                  // symbols per workgroup: kZprChunkSmall or kZprChunkLarge
+    int32_t nchunks;                // ceil(n / chunk), at least 1
     int32_t expected;               // blocks the stream must hold
     int32_t blocks_per_image;
     int32_t L;
     int32_t *counts;                // [nchunks] scratch: marker counts, then their exclusive prefix
-    uint32_t *ticket;               // scratch: workgroups of the count kernel that have finished
     int32_t *status;                // PIC_ZPR_ERR_* bits of the run
     // levels in stream order, i = 0 the coarsest (level k = L - 1 - i)
     int32_t first[PIC_MAX_LEVELS + 1];   // first block of stream level i inside an image

@@ -17,7 +17,6 @@ struct pic_zpr {
     int32_t max_chunks;
     int64_t scratch_bytes;
     int32_t *d_counts;          // [max_chunks]
-    uint32_t *d_ticket;         // one word, zero between runs
     // levels in stream order (coarsest first)
     int32_t first[PIC_MAX_LEVELS + 1];
     int32_t hk[PIC_MAX_LEVELS], wk[PIC_MAX_LEVELS], pw[PIC_MAX_LEVELS];
@@ -74,14 +73,14 @@ pic_status prepare(const pic_zpr *h, int32_t batch, const int32_t *symbols, int6
     p.sym = symbols;
     p.n = n_symbols;
     p.eob = eob;
-    p.nchunks = (int32_t)((n_symbols + pic::kZprChunk - 1) / pic::kZprChunk);
+    p.chunk = n_symbols >= pic::kZprLargeFrom ? pic::kZprChunkLarge : pic::kZprChunkSmall;
+    p.nchunks = (int32_t)((n_symbols + p.chunk - 1) / p.chunk);
     if (p.nchunks < 1)
         p.nchunks = 1;
     p.expected = (int32_t)blocks;
     p.blocks_per_image = (int32_t)h->blocks_per_image;
     p.L = h->desc.num_levels;
     p.counts = h->d_counts;
-    p.ticket = h->d_ticket;
     p.status = status;
     for (int i = 0; i <= p.L; ++i)
         p.first[i] = h->first[i];
@@ -131,7 +130,7 @@ pic_status pic_zpr_create(const pic_zpr_desc *d, pic_zpr **out)
     tmp.max_symbols = kMaxSymbolsPerBlock * nb * d->max_batch;
     if (tmp.max_symbols > kInt31)
         tmp.max_symbols = kInt31;
-    tmp.max_chunks = (int32_t)((tmp.max_symbols + pic::kZprChunk - 1) / pic::kZprChunk);
+    tmp.max_chunks = (int32_t)((tmp.max_symbols + pic::kZprChunkSmall - 1) / pic::kZprChunkSmall);
 
     pic_status st = check_device(&tmp.device);
     if (st != PIC_OK)
@@ -141,23 +140,15 @@ pic_status pic_zpr_create(const pic_zpr_desc *d, pic_zpr **out)
     if (!h)
         return PIC_E_NOMEM;
     *h = tmp;
-    // counts, then the arrival counter in its own 256-byte line
-    const size_t counts_bytes = ((size_t)h->max_chunks * sizeof(int32_t) + 255) & ~(size_t)255;
-    h->scratch_bytes = (int64_t)(counts_bytes + 256);
+    // per-chunk marker counts (every run writes them before reading them)
+    h->scratch_bytes = (int64_t)(((size_t)h->max_chunks * sizeof(int32_t) + 255) & ~(size_t)255);
     void *mem = nullptr;
     if (hipMalloc(&mem, (size_t)h->scratch_bytes) != hipSuccess) {
         (void)hipGetLastError();
         delete h;
         return PIC_E_HIP;
     }
-    if (hipMemset(mem, 0, (size_t)h->scratch_bytes) != hipSuccess) {
-        (void)hipGetLastError();
-        (void)hipFree(mem);
-        delete h;
-        return PIC_E_HIP;
-    }
     h->d_counts = static_cast<int32_t *>(mem);
-    h->d_ticket = reinterpret_cast<uint32_t *>(static_cast<char *>(mem) + counts_bytes);
     *out = h;
     return PIC_OK;
 }
@@ -213,7 +204,7 @@ pic_status pic_zpr_query(const pic_zpr *h, pic_zpr_info *info)
     info->blocks_per_image = h->blocks_per_image;
     info->max_symbols = h->max_symbols;
     info->scratch_bytes = h->scratch_bytes;
-    info->symbols_per_chunk = pic::kZprChunk;
+    info->symbols_per_chunk = pic::kZprChunkSmall;
     return PIC_OK;
 }
 

@@ -148,16 +148,31 @@ def test_negative_marker(orc):
     _check_decode(orc, H, W, L, 1, stream, eob)
 
 
-def test_marker_only_stream_spans_many_chunks(orc):
-    # every block empty: the stream is all markers (256 per chunk)
+@pytest.mark.parametrize("batch", [1, 40], ids=["short", "long"])
+def test_marker_only_stream_spans_many_chunks(orc, batch):
+    # every block empty: the stream is all markers (a full chunk of them each)
     H, W, L = 512, 768, 7
-    nb = orc.zpr_blocks(H, W, L)
+    nb = batch * orc.zpr_blocks(H, W, L)
     eob = 77
     stream = np.full(nb, eob, np.int32)
-    got, st = _gpu_decode(H, W, L, 1, stream, eob)
+    got, st = _gpu_decode(H, W, L, batch, stream, eob, fill=5.0)
     assert st == 0
     for g in got:
         assert not np.any(g)
+
+
+def test_long_stream_dense_blocks(orc):
+    # 1024-symbol chunks whose blocks are all 64 literals long (65 symbols)
+    H, W, L, batch = 256, 256, 3, 4
+    rng = np.random.default_rng(9)
+    nb = batch * orc.zpr_blocks(H, W, L)
+    co = pins_zpr.random_blocks(rng, nb, 1.0, 30)
+    eob = 30 + 17
+    stream = np.array([t for blk in co for t in pins_zpr.zpr_encode_block(blk, eob)], np.int32)
+    assert stream.size >= 262144
+    got, st = _gpu_expand(H, W, L, batch, stream, eob)
+    assert st == 0 and np.array_equal(got, co)
+    _check_decode(orc, H, W, L, batch, stream, eob)
 
 
 MALFORMED = ["missing_last_marker", "extra_marker", "trailing_symbols", "symbol_above_eob",
@@ -193,9 +208,14 @@ def _malformed(name, good, eob):
     raise KeyError(name)
 
 
+# (H, W, L, batch): a short stream (256-symbol chunks) and a long one (1024)
+MALFORMED_SHAPES = [(64, 96, 4, 2), (512, 768, 7, 6)]
+
+
+@pytest.mark.parametrize("shape", MALFORMED_SHAPES, ids=["short", "long"])
 @pytest.mark.parametrize("name", MALFORMED)
-def test_malformed_streams(orc, name):
-    H, W, L, batch = 64, 96, 4, 2
+def test_malformed_streams(orc, name, shape):
+    H, W, L, batch = shape
     s = synth.make_zpr_stream(H, W, L, batch, seed=7)
     stream = np.array(_malformed(name, s.symbols, s.eob), np.int32)
     _print_case("malformed", name, stream.size)
