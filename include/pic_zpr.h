@@ -100,7 +100,7 @@ PIC_API pic_status pic_zpr_create(const pic_zpr_desc *desc, pic_zpr **out);
  *               in block order (see above); may be NULL when n_symbols == 0.
  *   n_symbols : 0 .. min(65 * blocks_per_image * batch, 2^31 - 1) (a well-formed
  *               block has at most 64 symbols and its marker).
- *   eob       : the end-of-block marker, >= INT32_MIN + 17.
+ *   eob       : the end-of-block marker, in [INT32_MIN + 17, INT32_MAX - 1].
  *   latents   : host array of num_levels device pointers; latents[k] receives
  *               fp32 [batch][ceil(H/2^k)][ceil(W/2^k)] (the layout pic_decode_run
  *               reads).  Every sample of a well-formed stream is written;

@@ -38,10 +38,10 @@ namespace pic {
 namespace {
 
 constexpr int kWaves = kZprThreads / 64;
-constexpr int kHalo = 68;                    // >= 65 symbols before the chunk
+constexpr int kHalo = kZprThreads;           // symbols staged before the chunk (>= 65)
 constexpr int kGroups = kZprThreads / 8;     // blocks in flight per workgroup (8 lanes each)
-constexpr int kTile = 64 + 4;                // LDS words per 8x8 tile: the pad spreads the
-                                             // groups' tiles over different banks
+constexpr int kTile = 64 + 8;                // LDS words per 8x8 tile: the pad puts the 8
+                                             // groups' column reads on disjoint banks
 
 // JPEG zigzag scan (ITU-T T.81, Fig. A.6): entry p is the row-major index of
 // the p-th coefficient.
@@ -183,30 +183,59 @@ __global__ __launch_bounds__(kScanThreads) void k_zpr_scan(ZprParams p)
     }
 }
 
-// Inclusive sum over the 8-lane segment of x (lane gl = threadIdx.x & 7 of
-// its segment), with DPP row shifts: no LDS round trip.  row_shr:n reads the
-// lane n below within the 16-lane row; the gl >= n test drops what crosses
-// into the neighbouring segment.
-__device__ __forceinline__ int seg8_inclusive_sum(int x, int gl)
+// Coefficients one symbol produces (Alg. 1): 1 for a coefficient value
+// (s <= eob - 17), s - eob + 17 zeros for a run code (eob - 16 <= s < eob),
+// none for the marker or a symbol above it.  Clamping s into
+// [eob - 17, eob + 1] (one v_med3), d = clamped - (eob - 17) is 0 for a value, the run
+// length for a run code, 17 for the marker and 18 above it (no overflow: the
+// host keeps eob in [INT32_MIN + 17, INT32_MAX - 1]).
+__device__ __forceinline__ int zpr_coeffs(int32_t s, int32_t eob)
 {
-    int y = __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
-    x += gl >= 1 ? y : 0;
-    y = __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);       // row_shr:2
-    x += gl >= 2 ? y : 0;
-    y = __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);       // row_shr:4
-    x += gl >= 4 ? y : 0;
-    return x;
+    const int32_t lo = eob - 17, hi = eob + 1;
+    const int d = (s < lo ? lo : (s > hi ? hi : s)) - lo;
+    return d == 0 ? 1 : (d <= 16 ? d : 0);
+}
+
+// 8-point orthonormal inverse DCT, out[x] = sum_v in[v] a(v) cos((2x + 1) v pi / 16),
+// factored by the symmetries of the basis: out[x] and out[7 - x] are the sum
+// and difference of an even part (inputs v = 0, 2, 4, 6: a 4-point transform,
+// itself split into v = 0, 4 and v = 2, 6) and an odd part (v = 1, 3, 5, 7:
+// a 4 x 4 product).  35 operations instead of 64.
+__device__ __forceinline__ void idct8(const float in[8], float out[8])
+{
+    constexpr float A0 = dct_basis(0, 0), C4 = dct_basis(0, 4);
+    constexpr float C2 = dct_basis(0, 2), C6 = dct_basis(0, 6);
+    const float dc = in[0] * A0;
+    const float ee0 = __builtin_fmaf(in[4], C4, dc);     // rows x = 0, 3
+    const float ee1 = __builtin_fmaf(in[4], -C4, dc);    // rows x = 1, 2
+    const float eo0 = __builtin_fmaf(in[6], C6, in[2] * C2);
+    const float eo1 = __builtin_fmaf(in[6], -C2, in[2] * C6);
+    const float e[4] = {ee0 + eo0, ee1 + eo1, ee1 - eo1, ee0 - eo0};
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        float o = in[1] * dct_basis(x, 1);
+        o = __builtin_fmaf(in[3], dct_basis(x, 3), o);
+        o = __builtin_fmaf(in[5], dct_basis(x, 5), o);
+        o = __builtin_fmaf(in[7], dct_basis(x, 7), o);
+        out[x] = e[x] + o;
+        out[7 - x] = e[x] - o;
+    }
 }
 
 template <int CH, bool COEFF>
 __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
 {
-    constexpr int SPT = CH / kZprThreads;
-    __shared__ int32_t s_sym[kHalo + CH];
-    __shared__ int32_t s_pos[CH + 1];             // [0]: marker before the first block; [1 + r]: r-th marker
-    __shared__ __attribute__((aligned(16))) float s_blk[kGroups * kTile];   // S, then T in place
+    constexpr int NS = kHalo + CH;                 // staged symbols
+    constexpr int SPS = NS / kZprThreads;          // per thread, consecutive
+    static_assert(NS % kZprThreads == 0, "staging must divide evenly");
+    __shared__ int32_t s_sym[NS];
+    __shared__ int32_t s_cex[NS];                  // coefficients produced by the staged symbols before
+    __shared__ int16_t s_rid[NS];                  // chunk markers before the symbol: its block
+    __shared__ int32_t s_pos[CH + 1];              // [0]: marker before block 0; [1 + r]: block r's marker
+    __shared__ __attribute__((aligned(16))) float s_blk[kGroups * kTile];   // tiles: S, then T in place
     __shared__ uint8_t s_zz[64];
-    __shared__ int4 s_geo[PIC_MAX_LEVELS];        // stream level i: {h, w, patches per row, 0}
+    __shared__ int4 s_geo[PIC_MAX_LEVELS];         // stream level i: {h, w, pw | k << 16, ceil(2^k / pw)}
+    __shared__ int32_t s_first[PIC_MAX_LEVELS];
     __shared__ float *s_lat[PIC_MAX_LEVELS];
     __shared__ int32_t s_wsum[kWaves];
     __shared__ int32_t s_err;
@@ -214,40 +243,59 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     const int t = threadIdx.x, lane = t & 63;
     const int64_t cs = (int64_t)blockIdx.x * CH;
     const int32_t eob = p.eob;
+    const int32_t g0 = p.counts[blockIdx.x];       // blocks whose markers precede the chunk
 
-    // Stage the chunk and the symbols before it.  Positions before the stream
-    // act as markers (the first block starts at 0); positions past its end
-    // are never markers and never inside a block.
-    for (int i = t; i < kHalo + CH; i += kZprThreads) {
+    // Stage [cs - kHalo, cs + CH).  Positions before the stream act as markers
+    // (the first block starts at 0); positions past its end are never markers
+    // and never inside a block.
+    for (int i = t; i < NS; i += kZprThreads) {
         const int64_t gi = cs - kHalo + i;
         s_sym[i] = gi < 0 ? eob : (gi < p.n ? p.sym[gi] : 0);
     }
     if (t < 64)
         s_zz[t] = kZigzag[t];
     if (!COEFF && t < p.L) {
-        s_geo[t] = make_int4(p.hk[t], p.wk[t], p.pw[t], 0);
+        s_geo[t] = make_int4(p.hk[t], p.wk[t], p.pw[t] | p.pw_shift[t] << 16, p.pw_recip[t]);
+        s_first[t] = p.first[t];
         s_lat[t] = p.lat[t];
     }
     if (t == 0)
         s_err = 0;
     __syncthreads();
 
-    // Compact the chunk's marker positions (staged index) in stream order;
-    // thread t looks at the SPT consecutive symbols from t * SPT.
-    int32_t flags = 0, nm = 0;
+    // Every staged symbol once: the coefficients it produces and whether it
+    // is one of the chunk's markers.  One workgroup scan of both counts
+    // (packed: coefficients in the high half, markers in the low) gives each
+    // symbol its block (markers before it) and the coefficients produced
+    // before it, so a symbol's place in its block is a difference of two
+    // prefixes -- Alg. 1's running offset without a serial walk.
+    int c[SPS];
+    uint32_t mflags = 0;
+    int32_t csum = 0, nm = 0;
 #pragma unroll
-    for (int j = 0; j < SPT; ++j) {
-        const int k = t * SPT + j;
-        const bool mk = cs + k < p.n && s_sym[kHalo + k] == eob;
-        flags |= mk ? 1 << j : 0;
+    for (int j = 0; j < SPS; ++j) {
+        const int i = t * SPS + j;
+        const int32_t s = s_sym[i];
+        const int k = i - kHalo;
+        const bool mk = k >= 0 && cs + k < p.n && s == eob;
+        c[j] = zpr_coeffs(s, eob);
+        csum += c[j];
         nm += mk ? 1 : 0;
+        mflags |= mk ? 1u << j : 0u;
     }
-    int32_t m;
-    int32_t at = block_inclusive_sum(nm, s_wsum, &m) - nm;
+    int32_t total;
+    const int32_t incl = block_inclusive_sum(csum << 16 | nm, s_wsum, &total);
+    int32_t cpre = (incl >> 16) - csum, mpre = (incl & 0xffff) - nm;
+    const int m = total & 0xffff;
 #pragma unroll
-    for (int j = 0; j < SPT; ++j)
-        if (flags & (1 << j))
-            s_pos[1 + at++] = kHalo + t * SPT + j;
+    for (int j = 0; j < SPS; ++j) {
+        const int i = t * SPS + j;
+        s_cex[i] = cpre;
+        s_rid[i] = (int16_t)mpre;
+        cpre += c[j];
+        if (mflags >> j & 1u)
+            s_pos[1 + mpre++] = i;
+    }
     __syncthreads();
     if (m == 0)
         return;   // uniform: no block ends in this chunk
@@ -266,135 +314,107 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
         if (lane == 0)
             s_pos[0] = prev;
     }
-    __syncthreads();
 
-    // Eight lanes per block: lane gl holds symbols 8 gl .. 8 gl + 7 of it and,
-    // in the transform, row gl of the tile.
+    // Windows of kGroups blocks: zero the tiles, scatter the window's
+    // coefficient values through the zigzag table (any thread, any block),
+    // then eight lanes per block transform and store it.
     const int grp = t >> 3, gl = t & 7;
     float *blk = s_blk + grp * kTile;
-    float *tmp = blk;   // row gl of T replaces row gl of S, which only lane gl reads
-    const int32_t g0 = p.counts[blockIdx.x];        // blocks whose markers precede the chunk
     const int32_t img0 = g0 / p.blocks_per_image;
     const int32_t j0 = g0 - img0 * p.blocks_per_image;
     int err = 0;
     for (int r0 = 0; r0 < m; r0 += kGroups) {
+        reinterpret_cast<float4 *>(blk + gl * 8)[0] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        reinterpret_cast<float4 *>(blk + gl * 8)[1] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        __syncthreads();   // tiles zeroed (and s_pos[0] written, first round)
+        const int rend = r0 + kGroups < m ? r0 + kGroups : m;
+        const int lo = s_pos[r0] + 1, hi = s_pos[rend];
+        for (int i = lo + t; i < hi; i += kZprThreads) {
+            const int32_t s = s_sym[i];
+            const int r = s_rid[i];
+            if (g0 + r >= p.expected || s == eob)
+                continue;                            // a block past the stream's last, or a marker
+            if (s > eob) {
+                err |= PIC_ZPR_ERR_SYMBOL;           // skipped, as Alg. 1 has no code for it
+                continue;
+            }
+            if (s <= eob - 17) {                     // a coefficient value
+                const int pos = s_cex[i] - s_cex[s_pos[r] + 1];
+                if (pos < 64) {
+                    float *tile = s_blk + (r - r0) * kTile;
+                    if (COEFF)
+                        reinterpret_cast<int32_t *>(tile)[s_zz[pos]] = s;
+                    else
+                        tile[s_zz[pos]] = (float)s;
+                }
+            }
+        }
+        __syncthreads();   // the window's tiles are complete
+
         const int r = r0 + grp;
         const int32_t g = g0 + r;
-        if (r >= m || g >= p.expected)               // uniform over the 8 lanes of a block
-            continue;
-        const int end = s_pos[1 + r];
-        int begin = s_pos[r] + 1;
-        if (end - begin > 64) {
-            err |= PIC_ZPR_ERR_OVERFLOW;
-            begin = end - 64;
-        }
-        // Alg. 1 on this lane's eight symbols: coefficients each produces.
-        int32_t sv[8];
-        int cnt[8];
-        int tot = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int idx = begin + 8 * gl + e;
-            const bool in = idx < end;
-            const int32_t s = in ? s_sym[idx] : 0;
-            const bool over = in && s > eob;
-            const bool run = in && !over && s >= eob - 16;
-            const bool lit = in && s < eob - 16;
-            cnt[e] = run ? s - eob + 17 : (lit ? 1 : 0);
-            sv[e] = lit ? s : 0;                       // runs and padding write nothing
-            err |= over ? PIC_ZPR_ERR_SYMBOL : 0;
-            tot += cnt[e];
-        }
-        const int incl = seg8_inclusive_sum(tot, gl);
-        if (gl == 7 && incl > 64)
-            err |= PIC_ZPR_ERR_OVERFLOW;
-        int pos = incl - tot;
-
-        reinterpret_cast<float4 *>(blk)[2 * gl] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        reinterpret_cast<float4 *>(blk)[2 * gl + 1] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        asm volatile("" ::: "memory");
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            if (sv[e] != 0 && pos < 64) {
-                if (COEFF)
-                    reinterpret_cast<int32_t *>(blk)[s_zz[pos]] = sv[e];
-                else
-                    blk[s_zz[pos]] = (float)sv[e];
+        if (r < m && g < p.expected) {               // uniform over the 8 lanes of a block
+            if (gl == 0) {
+                const int end = s_pos[1 + r], begin = s_pos[r] + 1;
+                if (end - begin > 64 || s_cex[end] - s_cex[begin] > 64)
+                    err |= PIC_ZPR_ERR_OVERFLOW;
             }
-            pos += cnt[e];
-        }
-        asm volatile("" ::: "memory");
+            if (COEFF) {
+                const int4 *src = reinterpret_cast<const int4 *>(blk + gl * 8);
+                int4 *dst = reinterpret_cast<int4 *>(p.coeffs + (int64_t)g * 64 + gl * 8);
+                dst[0] = src[0];
+                dst[1] = src[1];
+                continue;
+            }
+            // Rows: lane gl transforms row gl and stores it in place; then it
+            // reads column gl (the LDS transpose) and transforms that.
+            const float4 sa = reinterpret_cast<const float4 *>(blk + gl * 8)[0];
+            const float4 sb = reinterpret_cast<const float4 *>(blk + gl * 8)[1];
+            const float S[8] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
+            float T[8];
+            idct8(S, T);
+            reinterpret_cast<float4 *>(blk + gl * 8)[0] = make_float4(T[0], T[1], T[2], T[3]);
+            reinterpret_cast<float4 *>(blk + gl * 8)[1] = make_float4(T[4], T[5], T[6], T[7]);
+            asm volatile("" ::: "memory");
+            float C[8], Z[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                C[u] = blk[u * 8 + gl];
+            idct8(C, Z);
+            asm volatile("" ::: "memory");
 
-        if (COEFF) {
-            const int4 *src = reinterpret_cast<const int4 *>(blk);
-            int4 *dst = reinterpret_cast<int4 *>(p.coeffs + (int64_t)g * 64);
-            dst[2 * gl] = src[2 * gl];
-            dst[2 * gl + 1] = src[2 * gl + 1];
-            continue;
-        }
-
-        // Rows: lane gl transforms row u = gl of S,
-        //   T[u][x] = sum_v S[u][v] a(v) cos((2x + 1) v pi / 16),
-        // and stores it; then it reads back column x = gl of T (the LDS
-        // transpose) and transforms it,
-        //   Z[y][x] = sum_u a(u) cos((2y + 1) u pi / 16) T[u][x].
-        const float4 sa = reinterpret_cast<const float4 *>(blk + gl * 8)[0];
-        const float4 sb = reinterpret_cast<const float4 *>(blk + gl * 8)[1];
-        const float S[8] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
-        float T[8];
+            // Un-patchify: image, level (stream order, found against the
+            // uniform first-block table), patch; lane gl writes column gl.
+            int32_t img = img0, j = j0 + r;
+            if (j >= p.blocks_per_image) {
+                const int32_t d = j / p.blocks_per_image;
+                img += d;
+                j -= d * p.blocks_per_image;
+            }
+            int lv = 0;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-            float acc = S[0] * dct_basis(x, 0);
-#pragma unroll
-            for (int v = 1; v < 8; ++v)
-                acc = __builtin_fmaf(S[v], dct_basis(x, v), acc);
-            T[x] = acc;
-        }
-        reinterpret_cast<float4 *>(tmp + gl * 8)[0] = make_float4(T[0], T[1], T[2], T[3]);
-        reinterpret_cast<float4 *>(tmp + gl * 8)[1] = make_float4(T[4], T[5], T[6], T[7]);
-        asm volatile("" ::: "memory");
-        float C[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            C[u] = tmp[u * 8 + gl];
-        float Z[8];
-#pragma unroll
-        for (int y = 0; y < 8; ++y) {
-            float acc = C[0] * dct_basis(y, 0);
-#pragma unroll
-            for (int u = 1; u < 8; ++u)
-                acc = __builtin_fmaf(C[u], dct_basis(y, u), acc);
-            Z[y] = acc;
-        }
-        asm volatile("" ::: "memory");
-
-        // Un-patchify: image, level (stream order, found against the uniform
-        // first-block table), patch; lane gl writes column gl of the patch.
-        int32_t img = img0, j = j0 + r;
-        if (j >= p.blocks_per_image) {
-            const int32_t d = j / p.blocks_per_image;
-            img += d;
-            j -= d * p.blocks_per_image;
-        }
-        int lv = 0;
-#pragma unroll
-        for (int i = 1; i < PIC_MAX_LEVELS; ++i)
-            lv += (i < p.L && j >= p.first[i]) ? 1 : 0;
-        const int4 geo = s_geo[lv];               // {h, w, patches per row, -}
-        float *base = s_lat[lv];
-        int32_t fl = 0;
-#pragma unroll
-        for (int i = 0; i < PIC_MAX_LEVELS; ++i)
-            fl = i == lv ? p.first[i] : fl;
-        const int32_t q = j - fl;
-        const int32_t py = q / geo.z, px = q - py * geo.z;
-        const int32_t col = px * 8 + gl;
-        if (col < geo.y) {
+            for (int i = 1; i < PIC_MAX_LEVELS; ++i)
+                lv += (i < p.L && j >= p.first[i]) ? 1 : 0;
+            const int4 geo = s_geo[lv];
+            float *base = s_lat[lv];
+            // q / pw as (q * ceil(2^k / pw)) >> k, k = 24 + ceil(log2 pw): exact
+            // for q < 2^24 (the handle refuses larger levels)
+            const uint32_t q = (uint32_t)(j - s_first[lv]);
+            const int32_t pwl = geo.z & 0xffff, sh = geo.z >> 16;
+            const int32_t py = (int32_t)(((uint64_t)q * (uint32_t)geo.w) >> sh);
+            const int32_t px = (int32_t)q - py * pwl;
+            const int32_t col = px * 8 + gl;
             float *dst = base + ((int64_t)img * geo.x + py * 8) * geo.y + col;
+            if (py * 8 + 8 <= geo.x && px * 8 + 8 <= geo.y) {      // whole patch inside the grid
 #pragma unroll
-            for (int y = 0; y < 8; ++y)
-                if (py * 8 + y < geo.x)
+                for (int y = 0; y < 8; ++y)
                     dst[(int64_t)y * geo.y] = Z[y];
+            } else if (col < geo.y) {
+#pragma unroll
+                for (int y = 0; y < 8; ++y)
+                    if (py * 8 + y < geo.x)
+                        dst[(int64_t)y * geo.y] = Z[y];
+            }
         }
     }
 

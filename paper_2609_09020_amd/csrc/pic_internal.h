@@ -72,6 +72,8 @@ struct ZprParams {
     int32_t hk[PIC_MAX_LEVELS];
     int32_t wk[PIC_MAX_LEVELS];
     int32_t pw[PIC_MAX_LEVELS];          // patches per row
+    int32_t pw_shift[PIC_MAX_LEVELS];    // k = 24 + ceil(log2 pw)
+    int32_t pw_recip[PIC_MAX_LEVELS];    // ceil(2^k / pw) (< 2^25): q / pw = (q * it) >> k for q < 2^24
     float *lat[PIC_MAX_LEVELS];          // [batch][hk][wk] of stream level i
     int32_t *coeffs;                     // [expected][64] row-major (expand only)
 };

@@ -56,7 +56,7 @@ pic_status prepare(const pic_zpr *h, int32_t batch, const int32_t *symbols, int6
         return PIC_E_INVALID;
     if ((uintptr_t)status % 4 || (n_symbols > 0 && (!symbols || (uintptr_t)symbols % 4)))
         return PIC_E_INVALID;
-    if (eob < INT32_MIN + 17)
+    if (eob < INT32_MIN + 17 || eob == INT32_MAX)
         return PIC_E_INVALID;
     const int64_t blocks = h->blocks_per_image * batch;
     int64_t cap = kMaxSymbolsPerBlock * blocks;
@@ -88,6 +88,11 @@ pic_status prepare(const pic_zpr *h, int32_t batch, const int32_t *symbols, int6
         p.hk[i] = h->hk[i];
         p.wk[i] = h->wk[i];
         p.pw[i] = h->pw[i];
+        int k = 24;
+        while ((1 << (k - 24)) < h->pw[i])
+            ++k;
+        p.pw_shift[i] = k;
+        p.pw_recip[i] = (int32_t)(((1ULL << k) + (uint64_t)h->pw[i] - 1) / (uint64_t)h->pw[i]);
     }
     return PIC_OK;
 }
@@ -124,6 +129,11 @@ pic_status pic_zpr_create(const pic_zpr_desc *d, pic_zpr **out)
         nb += (int64_t)((tmp.hk[i] + 7) / 8) * tmp.pw[i];
     }
     tmp.first[L] = (int32_t)nb;
+    // the kernels divide patch indices (< 2^24 per level) by patches per row
+    // (< 2^16) with a fixed-point reciprocal, exact in that range
+    for (int i = 0; i < L; ++i)
+        if (tmp.pw[i] >= (1 << 16) || tmp.first[i + 1] - tmp.first[i] >= (1 << 24))
+            return PIC_E_UNSUPPORTED;
     tmp.blocks_per_image = nb;
     if (nb * d->max_batch > kInt31)
         return PIC_E_UNSUPPORTED;

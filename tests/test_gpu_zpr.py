@@ -298,6 +298,7 @@ def test_argument_rejection():
         assert D.pic_zpr_expand(h, 1, p, 65 * bpi + 1, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
         assert D.pic_zpr_expand(h, 1, p, -1, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
         assert D.pic_zpr_expand(h, 1, p, 10, -2**31, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
+        assert D.pic_zpr_expand(h, 1, p, 10, 2**31 - 1, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
         assert D.pic_zpr_expand(h, 1, p, 10, 20, co.data_ptr() + 4, st.data_ptr()) == D.PIC_E_INVALID
         assert D.pic_zpr_expand(h, 1, p + 2, 10, 20, co.data_ptr(), st.data_ptr()) == D.PIC_E_INVALID
         assert D.pic_zpr_expand(h, 1, p, 10, 20, co.data_ptr(), 0) == D.PIC_E_INVALID
