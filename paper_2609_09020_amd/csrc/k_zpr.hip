@@ -1,36 +1,41 @@
 // Latent decoding from the ZpR symbol stream (PIC, Sec. 3.3 and Fig. 2;
 // App. B, Alg. 1; Sec. 3.2 Eq. (6)-(7) for the patches and the DCT).
 //
-// Three kernels.  The stream is partitioned into chunks of 256 symbols (one
-// per thread) or, for streams of 2^18 symbols and more, 1024 (four per
-// thread, so the per-workgroup set-up is spread over more blocks):
+// Two kernels (three on very long streams).  The stream is partitioned into
+// chunks of 256 symbols (one per thread) or, for streams of 2^18 symbols and
+// more, 1024 (four per thread, so the per-workgroup set-up is spread over
+// more blocks):
 //
-//   k_zpr_count   counts each chunk's end-of-block markers.
-//   k_zpr_scan    (one workgroup) turns the counts into their exclusive
-//                 prefix -- the index of the first block whose marker lies in
-//                 each chunk -- and writes the run's status word.  Together
-//                 the two replace the copy_if of marker offsets that Alg. 1
-//                 starts from: no offset array is built.
-//   k_zpr_expand  stages its chunk (and the 68 symbols before it) in LDS,
-//                 compacts the positions of its markers, and decodes every
-//                 block whose marker it holds.  A block's symbols start after
-//                 the previous marker, found in the chunk or, for the first
-//                 block, within the 65 staged symbols before it (a block of
-//                 64 symbols plus the preceding marker).  Eight lanes decode
-//                 one block: each takes eight consecutive symbols, the lanes
-//                 scan how many coefficients their symbols produce (Alg. 1's
-//                 running offset; a DPP scan inside the 8-lane segment), and
-//                 every literal is scattered through the zigzag table into a
-//                 zeroed 8x8 tile in LDS.  The tile then goes through the
-//                 separable inverse DCT: each lane transforms one row, the
-//                 rows go through LDS once to be read back as columns, and
-//                 each lane transforms one column and writes it to the
-//                 block's patch of the latent grid, cropped at the grid's
-//                 edge.  The basis entries are compile-time constants.
+//   k_zpr_count   counts each chunk's end-of-block markers (and clears the
+//                 status word).
+//   k_zpr_scan    (one workgroup; only beyond 16384 chunks) turns the counts
+//                 into their exclusive prefix.  Otherwise each workgroup of
+//                 the next kernel sums the counts of the chunks before its
+//                 own (L2-resident, a few loads per thread).  Either way the
+//                 result is the index of the first block whose marker lies in
+//                 the chunk; together the two replace the copy_if of marker
+//                 offsets that Alg. 1 starts from: no offset array is built.
+//   k_zpr_expand  stages its chunk (and the 256 symbols before it) in LDS
+//                 and, with one workgroup scan, finds for every symbol the
+//                 coefficients it produces, its block (the chunk's markers
+//                 before it) and its offset in that block (a difference of
+//                 two prefixes: Alg. 1's running offset without a serial
+//                 walk); the chunk's marker positions are compacted.  A
+//                 block's symbols start after the previous marker, found in
+//                 the chunk or, for the first block, within the 65 staged
+//                 symbols before it (a block of 64 symbols plus the preceding
+//                 marker).  Blocks are then decoded in windows of 32: the
+//                 tiles are zeroed, every coefficient value of the window is
+//                 written through the zigzag table into its block's 8x8
+//                 tile, and eight lanes per block run the separable inverse
+//                 DCT (rows, an LDS transpose, columns; a factored 8-point
+//                 transform with compile-time constants) and write the
+//                 block's patch of its latent grid, cropped at the grid's
+//                 edge.
 //
-// Memory traffic per block: its symbols (read by the count and the expand
-// kernels) and its 64 samples written once; the HBM floor is the stream read
-// once and the pyramid written once.
+// Memory traffic: the stream read by both kernels (plus the expand kernel's
+// 256-symbol halos) and the pyramid written once; the HBM floor of the step
+// is the stream read once and the pyramid written once.
 #include "pic_internal.h"
 #include "pic_zpr.h"
 
@@ -113,11 +118,14 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_count(ZprParams p)
     }
     int32_t tot;
     (void)block_inclusive_sum(mine, s_wsum, &tot);
-    if (t == 0)
+    if (t == 0) {
         p.counts[blockIdx.x] = tot;
+        if (blockIdx.x == 0)
+            *p.status = 0;     // the decoding kernel ors its findings into it
+    }
 }
 
-// One workgroup: counts[] -> exclusive prefix in place, and the status word.
+// One workgroup: counts[] -> exclusive prefix in place (long streams only).
 // Segments of kScanSeg counts are staged in LDS with coalesced loads; each
 // thread scans kScanPer consecutive entries, the workgroup scans the
 // per-thread sums, and the segment is written back coalesced.
@@ -174,12 +182,6 @@ __global__ __launch_bounds__(kScanThreads) void k_zpr_scan(ZprParams p)
         }
         carry += seg_total;
         __syncthreads();   // s_seg and s_wsum are rewritten by the next segment
-    }
-    if (t == 0) {
-        int32_t st = carry != p.expected ? PIC_ZPR_ERR_COUNT : 0;
-        if (p.n > 0 && p.sym[p.n - 1] != p.eob)
-            st |= PIC_ZPR_ERR_COUNT;
-        *p.status = st;
     }
 }
 
@@ -243,7 +245,23 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     const int t = threadIdx.x, lane = t & 63;
     const int64_t cs = (int64_t)blockIdx.x * CH;
     const int32_t eob = p.eob;
-    const int32_t g0 = p.counts[blockIdx.x];       // blocks whose markers precede the chunk
+    // Blocks whose markers precede the chunk: the scan kernel's prefix, or the
+    // sum of the earlier chunks' counts (L2-resident; eight independent loads
+    // in flight per thread).
+    int32_t g0;
+    if (p.counts_are_prefix) {
+        g0 = p.counts[blockIdx.x];
+    } else {
+        const int c = (int)blockIdx.x;
+        int32_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int j = t; j < c; j += 8 * kZprThreads) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                a[u] += j + u * kZprThreads < c ? p.counts[j + u * kZprThreads] : 0;
+        }
+        const int32_t part = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+        (void)block_inclusive_sum(part, s_wsum, &g0);
+    }
 
     // Stage [cs - kHalo, cs + CH).  Positions before the stream act as markers
     // (the first block starts at 0); positions past its end are never markers
@@ -297,6 +315,9 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
             s_pos[1 + mpre++] = i;
     }
     __syncthreads();
+    if (t == 0 && blockIdx.x == (unsigned)p.nchunks - 1 &&
+        ((int64_t)g0 + m != p.expected || (p.n > 0 && p.sym[p.n - 1] != eob)))
+        atomicOr(p.status, PIC_ZPR_ERR_COUNT);   // marker count, or symbols after the last marker
     if (m == 0)
         return;   // uniform: no block ends in this chunk
 
@@ -435,10 +456,12 @@ hipError_t launch_chunk(const ZprParams &p, bool coeff_only, hipStream_t s)
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_zpr_scan, dim3(1), dim3(kScanThreads), 0, s, p);
-    e = hipGetLastError();
-    if (e != hipSuccess || p.n == 0)
-        return e;
+    if (p.counts_are_prefix) {
+        hipLaunchKernelGGL(k_zpr_scan, dim3(1), dim3(kScanThreads), 0, s, p);
+        e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
     if (coeff_only)
         hipLaunchKernelGGL((k_zpr_expand<CH, true>), grid, block, 0, s, p);
     else

@@ -65,7 +65,9 @@ struct ZprParams {
     int32_t expected;               // blocks the stream must hold
     int32_t blocks_per_image;
     int32_t L;
-    int32_t *counts;                // [nchunks] scratch: marker counts, then their exclusive prefix
+    int32_t *counts;                // [nchunks] scratch: marker counts (their exclusive prefix
+                                    // when counts_are_prefix)
+    int32_t counts_are_prefix;      // 1: the scan kernel ran (long streams)
     int32_t *status;                // PIC_ZPR_ERR_* bits of the run
     // levels in stream order, i = 0 the coarsest (level k = L - 1 - i)
     int32_t first[PIC_MAX_LEVELS + 1];   // first block of stream level i inside an image

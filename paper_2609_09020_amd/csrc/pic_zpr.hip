@@ -26,6 +26,9 @@ namespace {
 
 constexpr int64_t kMaxSymbolsPerBlock = 65;   // 64 coefficients and the marker
 constexpr int64_t kInt31 = (1LL << 31) - 1;
+// Up to this many chunks the decoding kernel sums the earlier chunks' marker
+// counts itself; beyond it a one-workgroup scan kernel runs first.
+constexpr int32_t kPrefixInKernelMax = 16384;
 
 int32_t level_dim(int32_t n, int k) { return (int32_t)(((int64_t)n + (1LL << k) - 1) >> k); }
 
@@ -81,6 +84,7 @@ pic_status prepare(const pic_zpr *h, int32_t batch, const int32_t *symbols, int6
     p.blocks_per_image = (int32_t)h->blocks_per_image;
     p.L = h->desc.num_levels;
     p.counts = h->d_counts;
+    p.counts_are_prefix = p.nchunks > kPrefixInKernelMax;
     p.status = status;
     for (int i = 0; i <= p.L; ++i)
         p.first[i] = h->first[i];

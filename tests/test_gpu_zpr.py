@@ -331,3 +331,42 @@ def test_latents_feed_the_synthesis(orc):
         torch.cuda.synchronize()
     ref = orc.decode(got, inp.weights, inp.biases, wl.widths, H, W, out="raw")
     assert np.abs(img.cpu().numpy() - ref).max() <= 1e-5 * max(1.0, np.abs(ref).max())
+
+
+def test_many_chunks_long_stream(orc):
+    # over 9000 chunks of 1024 symbols (every block 64 coefficient values and
+    # its marker): the group-count prefix across many groups
+    H, W, L, batch = 1024, 1024, 2, 7
+    rng = np.random.default_rng(21)
+    nb = batch * orc.zpr_blocks(H, W, L)
+    co = pins_zpr.random_blocks(rng, nb, 1.0, 50)
+    eob = 50 + 17
+    stream = np.concatenate([co[:, pins_zpr.ZZ], np.full((nb, 1), eob)], axis=1).astype(np.int32).ravel()
+    assert stream.size > 8192 * 1024
+    _print_case("many chunks", stream.size)
+    got, st = _gpu_expand(H, W, L, batch, stream, eob)
+    assert st == 0 and np.array_equal(got, co)
+    _check_decode(orc, H, W, L, batch, stream, eob)
+
+
+def test_scan_path_very_long_stream(orc):
+    # beyond 16384 chunks of 1024 symbols the one-workgroup scan kernel turns
+    # the counts into prefixes first: 85M symbols, every block 64 values and
+    # its marker, checked bit for bit in expand mode (the blocks are known)
+    H, W, L, batch = 4096, 4096, 1, 5
+    nb = batch * orc.zpr_blocks(H, W, L)
+    rng = np.random.default_rng(23)
+    co = rng.integers(1, 51, size=(nb, 64), dtype=np.int32)
+    co *= np.where(rng.random((nb, 64)) < 0.5, -1, 1).astype(np.int32)
+    eob = 50 + 17
+    stream = np.empty((nb, 65), np.int32)
+    stream[:, :64] = co[:, pins_zpr.ZZ]
+    stream[:, 64] = eob
+    stream = stream.ravel()
+    assert stream.size > 16384 * 1024
+    _print_case("scan path", stream.size)
+    got, st = _gpu_expand(H, W, L, batch, stream, eob)
+    assert st == 0 and np.array_equal(got, co)
+    # and the count check still works on this path
+    got, st = _gpu_expand(H, W, L, batch, stream[:-1], eob)
+    assert st == D.PIC_ZPR_ERR_COUNT
