@@ -3,8 +3,9 @@
 Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product library neither imports nor
 links it.  It wraps ``pic_oracle.c`` (the synthesis step: plain C, fp64 and an fp32
-model) and ``zpr_oracle.c`` (latents from the ZpR symbol stream, fp64) with
-numpy marshalling; the arithmetic lives in the C files (see their headers).
+model), ``zpr_oracle.c`` (latents from the ZpR symbol stream, fp64) and
+``huff_oracle.c`` (symbols from the Huffman bitstream) with numpy
+marshalling; the arithmetic lives in the C files (see their headers).
 """
 from __future__ import annotations
 
@@ -57,6 +58,13 @@ def _bind(path):
     lib.pic_oracle_zpr_decode_f64.restype = ctypes.c_int
     lib.pic_oracle_zpr_decode_f64.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_long,
                                                                     ctypes.c_int32, ctypes.c_void_p]
+    # entropy decoding (huff_oracle.c)
+    lib.pic_oracle_huffman_codes.restype = ctypes.c_int
+    lib.pic_oracle_huffman_codes.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    lib.pic_oracle_huffman_decode.restype = ctypes.c_int
+    lib.pic_oracle_huffman_decode.argtypes = [ctypes.c_void_p, ctypes.c_long, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int, ctypes.c_long, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p]
     return lib
 
 
@@ -229,6 +237,30 @@ class Oracle:
         if err < 0:
             raise ValueError("oracle rejected the arguments")
         return self._split_levels(flat, H, W, L, batch), int(err)
+
+    # ---------------------------------------------- Huffman bitstream -> symbols
+
+    def huffman_codes(self, lengths) -> tuple:
+        """Canonical codes of the given lengths: (codes uint32 [n], error flags)."""
+        ln = np.ascontiguousarray(lengths, dtype=np.uint8)
+        codes = np.zeros(max(ln.size, 1), dtype=np.uint32)
+        err = self._lib.pic_oracle_huffman_codes(ln.ctypes.data, ln.size, codes.ctypes.data)
+        return codes[:ln.size], int(err)
+
+    def huffman_decode(self, data, n_bits: int, values, lengths, n_out: int) -> tuple:
+        """Decode n_out symbols from the MSB-first bitstream `data` (bytes or
+        uint8 array; its first n_bits bits): (symbols int32 [decoded], error
+        flags, bits used)."""
+        buf = np.frombuffer(bytes(data), dtype=np.uint8) if not isinstance(data, np.ndarray) else \
+            np.ascontiguousarray(data, dtype=np.uint8)
+        vals = np.ascontiguousarray(values, dtype=np.int32)
+        ln = np.ascontiguousarray(lengths, dtype=np.uint8)
+        out = np.zeros(max(int(n_out), 1), dtype=np.int32)
+        nd, used = ctypes.c_long(0), ctypes.c_long(0)
+        err = self._lib.pic_oracle_huffman_decode(buf.ctypes.data if buf.size else None, int(n_bits),
+                                                  vals.ctypes.data, ln.ctypes.data, ln.size, int(n_out),
+                                                  out.ctypes.data, ctypes.byref(nd), ctypes.byref(used))
+        return out[:nd.value], int(err), int(used.value)
 
     def decode_inputs(self, inp, out: str = "clamped", precision: str = "f64",
                       nthreads: int = 0, batch_slice: slice = None, rows: tuple = None) -> np.ndarray:

@@ -13,7 +13,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "pic_oracle.c")
 ZPR_SRC = os.path.join(HERE, "zpr_oracle.c")
-SRCS = (SRC, ZPR_SRC)
+HUFF_SRC = os.path.join(HERE, "huff_oracle.c")
+SRCS = (SRC, ZPR_SRC, HUFF_SRC)
 LIB = os.path.join(HERE, "libpic_oracle.so")
 
 

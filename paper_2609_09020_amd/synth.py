@@ -303,3 +303,86 @@ def workload_zpr_stream(w: Workload, batch: Optional[int] = None, seed: Optional
     """The symbol stream of a named workload's pyramid shape."""
     return make_zpr_stream(w.height, w.width, w.levels, w.batch if batch is None else batch,
                            w.seed + 1000 if seed is None else seed)
+
+
+# ------------------------------------------------------------ Huffman streams
+#
+# The bitstream the entropy decoder reads (PIC, Sec. 3.3: an image-specific
+# Huffman code whose stored table lists only the symbols used).  Format, as
+# the decoder takes it: a table of (symbol value, code length) pairs, one per
+# distinct symbol in increasing value order; the canonical code of those
+# lengths (codes of one length consecutive in table order, shorter lengths
+# first); the codewords packed most significant bit first.  The generator
+# draws nothing new: it codes a ZpR stream with a Huffman code built from
+# that stream's own symbol histogram (the two rarest subtrees merged
+# repeatedly), its longest codeword kept at or below max_len bits by raising
+# the rarest counts.
+
+
+@dataclass
+class HuffStream:
+    """One entropy-decoding call's input."""
+
+    data: np.ndarray            # uint8 [ceil(n_bits / 8)], MSB first
+    n_bits: int
+    values: np.ndarray          # int32 [n_table], increasing
+    lengths: np.ndarray         # uint8 [n_table]
+    n_symbols: int
+    symbols: np.ndarray         # int32 [n_symbols]: what the bits code
+
+
+def _huff_depths(freqs):
+    import heapq
+    n = len(freqs)
+    if n == 1:
+        return np.ones(1, dtype=np.int64)
+    depth = np.zeros(n, dtype=np.int64)
+    heap = [(int(f), i, (i,)) for i, f in enumerate(freqs)]
+    heapq.heapify(heap)
+    uid = n
+    while len(heap) > 1:
+        f1, _, a = heapq.heappop(heap)
+        f2, _, b = heapq.heappop(heap)
+        members = a + b
+        depth[list(members)] += 1
+        heapq.heappush(heap, (f1 + f2, uid, members))
+        uid += 1
+    return depth
+
+
+def make_huff_stream(symbols: np.ndarray, max_len: int = 20) -> HuffStream:
+    """Huffman-code `symbols` (int32) with a code built from their histogram."""
+    symbols = np.ascontiguousarray(symbols, dtype=np.int32)
+    values, inverse, counts = np.unique(symbols, return_inverse=True, return_counts=True)
+    floor = 0
+    while True:
+        depth = _huff_depths(np.maximum(counts, floor))
+        if depth.max() <= max_len:
+            break
+        floor = max(1, floor * 2, int(counts.sum()) >> (max_len - 2))
+    lengths = depth.astype(np.int64)
+    # canonical codes: by (length, table order)
+    order = np.lexsort((np.arange(lengths.size), lengths))
+    codes = np.zeros(lengths.size, dtype=np.int64)
+    code, prev = 0, int(lengths[order[0]])
+    for k, i in enumerate(order):
+        if k:
+            code = (code + 1) << (int(lengths[i]) - prev)
+        codes[i] = code
+        prev = int(lengths[i])
+    ln = lengths[inverse]
+    cw = codes[inverse]
+    start = np.concatenate([[0], np.cumsum(ln)[:-1]])
+    n_bits = int(ln.sum())
+    bitarr = np.zeros(n_bits + (-n_bits % 8), dtype=np.uint8)
+    for j in range(int(lengths.max())):
+        sel = ln > j
+        bitarr[start[sel] + j] = (cw[sel] >> (ln[sel] - 1 - j)) & 1
+    data = np.packbits(bitarr)
+    return HuffStream(data, n_bits, values.astype(np.int32), lengths.astype(np.uint8), int(symbols.size),
+                      symbols)
+
+
+def workload_huff_stream(w: Workload, batch: Optional[int] = None, seed: Optional[int] = None) -> HuffStream:
+    """The Huffman bitstream of a named workload's ZpR stream."""
+    return make_huff_stream(workload_zpr_stream(w, batch, seed).symbols)

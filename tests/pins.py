@@ -380,3 +380,8 @@ ALL_CHECKS = [check_level_dims, check_upsample_constant, check_upsample_affine,
 from tests.pins_zpr import ZPR_CHECKS  # noqa: E402
 
 ALL_CHECKS += ZPR_CHECKS
+
+# the entropy-decoding step (Huffman bitstream -> symbols): pins_huff.py
+from tests.pins_huff import HUFF_CHECKS  # noqa: E402
+
+ALL_CHECKS += HUFF_CHECKS

@@ -68,6 +68,18 @@ ZPR_MUTANTS = [
     ("no_symbol_count_limit", "if (produced > 64 || end - begin > 64)", "if (produced > 64)"),
 ]
 
+# the same for huff_oracle.c (symbols from the Huffman bitstream)
+HUFF_MUTANTS = [
+    ("lsb_first", "(bits[pos >> 3] >> (7 - (pos & 7))) & 1u", "(bits[pos >> 3] >> (pos & 7)) & 1u"),
+    ("canonical_no_shift", "code = (code + (uint32_t)count[l - 1]) << 1;", "code = code + (uint32_t)count[l - 1];"),
+    ("canonical_count_off_by_one", "code = (code + (uint32_t)count[l - 1]) << 1;",
+     "code = (code + (uint32_t)count[l]) << 1;"),
+    ("kraft_unchecked", "if (kraft > (1LL << HO_MAX_LEN))\n        return HO_ERR_TABLE;", ""),
+    ("match_ignores_length", "if (lengths[i] == len && codes[i] == acc) {", "if (codes[i] == acc) {"),
+    ("no_prefix_check", "if (found < 0 && !longer) {", "if (0) {"),
+    ("value_is_index", "out[s] = values[found];", "out[s] = found;"),
+]
+
 
 def _caught(orc):
     for check in pins.ALL_CHECKS:
@@ -78,7 +90,8 @@ def _caught(orc):
     return None
 
 
-CASES = [(obuild.SRC,) + m for m in MUTANTS] + [(obuild.ZPR_SRC,) + m for m in ZPR_MUTANTS]
+CASES = ([(obuild.SRC,) + m for m in MUTANTS] + [(obuild.ZPR_SRC,) + m for m in ZPR_MUTANTS] +
+         [(obuild.HUFF_SRC,) + m for m in HUFF_MUTANTS])
 
 
 @pytest.mark.parametrize("path,name,old,new", CASES, ids=[c[1] for c in CASES])
