@@ -85,3 +85,42 @@ struct ZprParams {
 hipError_t launch_zpr(const ZprParams &p, bool coeff_only, hipStream_t s);
 
 }  // namespace pic
+
+// ------------------------------------------------------------------------
+// Huffman entropy decoding (k_huff.hip, pic_huff.hip).
+namespace pic {
+
+constexpr int kHuffThreads = 256;
+constexpr int kHuffSub = 128;                  // bitstream bits per parsing thread
+constexpr int kHuffLutBits = 11;               // first-level decode table: 2^11 entries
+constexpr int kHuffMaxLen = 24;
+constexpr int kHuffMaxTable = 4096;
+
+// Kernel argument of the entropy-decoding kernels.
+struct HuffParams {
+    const uint8_t *data;            // bitstream, MSB first
+    int32_t n_bits;
+    int32_t nsub;                   // subsequences: ceil(n_bits / kHuffSub), at least 1
+    int32_t n_symbols;              // symbols to decode
+    int32_t n_table;
+    const int32_t *values;          // [n_table]
+    const uint8_t *lengths;         // [n_table]
+    int32_t *out;                   // [n_symbols]
+    int32_t *status;
+    // scratch
+    uint32_t *lut;                  // [1 << kHuffLutBits]: index | length << 16, 0 = longer code
+    int32_t *tab;                   // [0]: table valid, [1]: longest length,
+                                    // [8 + l]: first code, [40 + l]: count, [72 + l]: first index of length l
+    int32_t *sorted;                // [kHuffMaxTable] symbol values in code order
+    uint32_t *mask;                 // [nsub][4]: codeword starts of the parse from the subsequence's start
+    int32_t *end;                   // [nsub]: where that parse crosses into the next subsequence, -1 if it
+                                    // met a pattern that is no codeword
+    uint32_t *fail;                 // [nsub / 32 rounded up to 2]: subsequences whose parse missed the true start
+    int32_t *flags;                 // [0]: some subsequence was out of step; [1]: first subsequence
+                                    // whose true parse meets a pattern that is no codeword
+    int32_t *blk;                   // [ceil(nsub / kHuffThreads)]: symbols per block of subsequences
+};
+
+hipError_t launch_huff(const HuffParams &p, hipStream_t s);
+
+}  // namespace pic

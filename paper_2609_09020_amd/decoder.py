@@ -1,11 +1,12 @@
 """Thin ctypes binding of libpic_decode.so (include/pic_decode.h).
 
-The ``pic_decode_*``, ``pic_zpr_*``, ``pic_fuse_modulation`` and
+The ``pic_decode_*``, ``pic_zpr_*``, ``pic_huff_*``, ``pic_fuse_modulation`` and
 ``pic_status_string`` functions mirror the C entry points one to one and only
 marshal arguments; every step runs in the HIP kernels behind them.
-``Decoder`` (synthesis) and ``ZprDecoder`` (latents from the ZpR symbol
-stream) wrap handles for use with torch tensors (torch supplies device memory
-and streams, nothing else).
+``Decoder`` (synthesis), ``ZprDecoder`` (latents from the ZpR symbol stream)
+and ``HuffDecoder`` (ZpR symbols from the Huffman bitstream) wrap handles for
+use with torch tensors (torch supplies device memory and streams, nothing
+else).
 
 There is no fallback: if the library is missing or fails to load, every call
 raises.
@@ -32,7 +33,11 @@ VARIANT_NAMES = {v: k for k, v in VARIANTS.items()}
 # Every symbol include/pic_decode.h and include/pic_zpr.h declare.
 EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_run_layers", "pic_decode_query",
            "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation",
-           "pic_zpr_create", "pic_zpr_decode", "pic_zpr_expand", "pic_zpr_query", "pic_zpr_destroy")
+           "pic_zpr_create", "pic_zpr_decode", "pic_zpr_expand", "pic_zpr_query", "pic_zpr_destroy",
+           "pic_huff_create", "pic_huff_decode", "pic_huff_query", "pic_huff_destroy")
+
+PIC_HUFF_ERR_BITS, PIC_HUFF_ERR_CODE, PIC_HUFF_ERR_TABLE = 1, 2, 4
+PIC_HUFF_MAX_LEN, PIC_HUFF_MAX_TABLE = 24, 4096
 
 PIC_ZPR_ERR_COUNT, PIC_ZPR_ERR_OVERFLOW, PIC_ZPR_ERR_SYMBOL = 1, 2, 4
 
@@ -63,6 +68,16 @@ class pic_zpr_info(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("device", ctypes.c_int32),
                 ("blocks_per_image", ctypes.c_int64), ("max_symbols", ctypes.c_int64),
                 ("scratch_bytes", ctypes.c_int64), ("symbols_per_chunk", ctypes.c_int32)]
+
+
+class pic_huff_desc(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("reserved", ctypes.c_int32), ("max_bits", ctypes.c_int64)]
+
+
+class pic_huff_info(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("device", ctypes.c_int32), ("max_bits", ctypes.c_int64),
+                ("scratch_bytes", ctypes.c_int64), ("bits_per_thread", ctypes.c_int32),
+                ("lut_bits", ctypes.c_int32)]
 
 
 class PicError(RuntimeError):
@@ -115,6 +130,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pic_zpr_query.argtypes = [ctypes.c_void_p, ctypes.POINTER(pic_zpr_info)]
     lib.pic_zpr_destroy.restype = None
     lib.pic_zpr_destroy.argtypes = [ctypes.c_void_p]
+    lib.pic_huff_create.restype = ctypes.c_int
+    lib.pic_huff_create.argtypes = [ctypes.POINTER(pic_huff_desc), ctypes.POINTER(ctypes.c_void_p)]
+    lib.pic_huff_decode.restype = ctypes.c_int
+    lib.pic_huff_decode.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_huff_query.restype = ctypes.c_int
+    lib.pic_huff_query.argtypes = [ctypes.c_void_p, ctypes.POINTER(pic_huff_info)]
+    lib.pic_huff_destroy.restype = None
+    lib.pic_huff_destroy.argtypes = [ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -269,6 +294,43 @@ def pic_zpr_query(handle: int) -> dict:
 
 def pic_zpr_destroy(handle: int) -> None:
     load_library().pic_zpr_destroy(handle)
+
+
+def make_huff_desc(max_bits: int) -> pic_huff_desc:
+    d = pic_huff_desc()
+    d.struct_size = ctypes.sizeof(pic_huff_desc)
+    d.max_bits = int(max_bits)
+    return d
+
+
+def pic_huff_create(desc: pic_huff_desc) -> int:
+    """Returns the handle (an integer address); raises PicError."""
+    h = ctypes.c_void_p()
+    st = load_library().pic_huff_create(ctypes.byref(desc), ctypes.byref(h))
+    if st != PIC_OK:
+        raise PicError(st, "pic_huff_create")
+    return h.value
+
+
+def pic_huff_decode(handle: int, data_ptr: int, n_bits: int, values_ptr: int, lengths_ptr: int, n_table: int,
+                    n_symbols: int, out_ptr: int, status_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call; returns the status (no raise, for argument tests)."""
+    return load_library().pic_huff_decode(handle, data_ptr, int(n_bits), values_ptr, lengths_ptr, int(n_table),
+                                          int(n_symbols), out_ptr, status_ptr, stream)
+
+
+def pic_huff_query(handle: int) -> dict:
+    info = pic_huff_info()
+    info.struct_size = ctypes.sizeof(pic_huff_info)
+    st = load_library().pic_huff_query(handle, ctypes.byref(info))
+    if st != PIC_OK:
+        raise PicError(st, "pic_huff_query")
+    return dict(device=info.device, max_bits=info.max_bits, scratch_bytes=info.scratch_bytes,
+                bits_per_thread=info.bits_per_thread, lut_bits=info.lut_bits)
+
+
+def pic_huff_destroy(handle: int) -> None:
+    load_library().pic_huff_destroy(handle)
 
 
 # ------------------------------------------------------------ torch layer
@@ -479,6 +541,68 @@ class ZprDecoder:
     def close(self):
         if getattr(self, "handle", None):
             pic_zpr_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+class HuffDecoder:
+    """One entropy-decoding handle (include/pic_huff.h).
+
+    ``decode`` takes the bitstream (contiguous uint8 device tensor, MSB
+    first), its bit count, the code table (int32 values and uint8 lengths,
+    device tensors) and the number of symbols, and returns the symbols (int32
+    device tensor, the input of ``ZprDecoder``) and a one-element int32 status
+    tensor (PIC_HUFF_ERR_* bits).  It enqueues on torch's current stream (or
+    ``stream``) and does not synchronise.
+    """
+
+    def __init__(self, max_bits: int):
+        self.max_bits = int(max_bits)
+        self.handle = pic_huff_create(make_huff_desc(max_bits))
+
+    def info(self) -> dict:
+        return pic_huff_query(self.handle)
+
+    def decode(self, data, n_bits: int, values, lengths, n_symbols: int, out=None, status=None, stream=None):
+        import torch
+        dev = values.device
+        if data.dtype != torch.uint8 or not data.is_contiguous() or data.device != dev or \
+                data.numel() * 8 < int(n_bits):
+            raise ValueError("data: need a contiguous uint8 device tensor holding n_bits bits")
+        if values.dtype != torch.int32 or not values.is_contiguous() or values.device.type != "cuda":
+            raise ValueError("values: need a contiguous int32 device tensor")
+        if lengths.dtype != torch.uint8 or not lengths.is_contiguous() or lengths.device != dev or \
+                lengths.numel() != values.numel():
+            raise ValueError("lengths: need a contiguous uint8 device tensor like values")
+        if out is None:
+            out = torch.empty(max(int(n_symbols), 1), dtype=torch.int32, device=dev)
+        if out.dtype != torch.int32 or not out.is_contiguous() or out.device != dev or out.numel() < n_symbols:
+            raise ValueError("out: need a contiguous int32 device tensor of n_symbols entries")
+        if status is None:
+            status = torch.empty(1, dtype=torch.int32, device=dev)
+        if stream is None:
+            stream = torch.cuda.current_stream(dev).cuda_stream
+        st = pic_huff_decode(self.handle, data.data_ptr() if data.numel() else 0, n_bits, values.data_ptr(),
+                             lengths.data_ptr(), values.numel(), n_symbols, out.data_ptr(), status.data_ptr(),
+                             int(stream))
+        if st != PIC_OK:
+            raise PicError(st, "pic_huff_decode")
+        return out[:int(n_symbols)], status
+
+    def close(self):
+        if getattr(self, "handle", None):
+            pic_huff_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

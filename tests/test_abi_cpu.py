@@ -14,7 +14,7 @@ from paper_2609_09020_amd import decoder as D
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "pic_decode.h")
-HEADERS = [HEADER, os.path.join(ROOT, "include", "pic_zpr.h")]
+HEADERS = [HEADER, os.path.join(ROOT, "include", "pic_zpr.h"), os.path.join(ROOT, "include", "pic_huff.h")]
 
 
 def _declared():
@@ -210,3 +210,50 @@ def test_zpr_nodevice_on_cpu_host():
     with pytest.raises(pkg.PicError) as e:
         pkg.ZprDecoder(64, 64, 4)
     assert e.value.status == D.PIC_E_NODEVICE
+
+
+def test_huff_struct_layout_matches_header(tmp_path):
+    src = tmp_path / "layout_huff.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "pic_huff.h"\n'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(pic_huff_desc),'
+                   ' offsetof(pic_huff_desc, max_bits), sizeof(pic_huff_info),'
+                   ' offsetof(pic_huff_info, scratch_bytes), offsetof(pic_huff_info, bits_per_thread),'
+                   ' offsetof(pic_huff_info, lut_bits));'
+                   'printf("%d %d %d %d %d\\n", PIC_HUFF_ERR_BITS, PIC_HUFF_ERR_CODE, PIC_HUFF_ERR_TABLE,'
+                   ' PIC_HUFF_MAX_LEN, PIC_HUFF_MAX_TABLE);return 0;}\n')
+    exe = tmp_path / "layout_huff"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(D.pic_huff_desc), D.pic_huff_desc.max_bits.offset, ctypes.sizeof(D.pic_huff_info),
+            D.pic_huff_info.scratch_bytes.offset, D.pic_huff_info.bits_per_thread.offset,
+            D.pic_huff_info.lut_bits.offset, D.PIC_HUFF_ERR_BITS, D.PIC_HUFF_ERR_CODE, D.PIC_HUFF_ERR_TABLE,
+            D.PIC_HUFF_MAX_LEN, D.PIC_HUFF_MAX_TABLE]
+    assert got == want
+
+
+@pytest.mark.parametrize("raw", [dict(max_bits=0), dict(max_bits=2**31), dict(struct_size=4), dict(reserved=1)])
+def test_huff_invalid_descriptors(raw):
+    desc = D.make_huff_desc(1 << 20)
+    for k, v in raw.items():
+        setattr(desc, k, v)
+    h = ctypes.c_void_p()
+    assert pkg.load_library().pic_huff_create(ctypes.byref(desc), ctypes.byref(h)) == D.PIC_E_INVALID
+    assert h.value is None
+
+
+def test_huff_null_arguments():
+    lib = pkg.load_library()
+    assert lib.pic_huff_create(None, None) == D.PIC_E_INVALID
+    assert D.pic_huff_decode(None, 4096, 8, 4096, 4096, 1, 1, 4096, 4096) == D.PIC_E_INVALID
+    info = D.pic_huff_info()
+    info.struct_size = ctypes.sizeof(D.pic_huff_info)
+    assert lib.pic_huff_query(None, ctypes.byref(info)) == D.PIC_E_INVALID
+    lib.pic_huff_destroy(None)
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_huff_nodevice_on_cpu_host():
+    h = ctypes.c_void_p()
+    desc = D.make_huff_desc(1 << 20)
+    assert pkg.load_library().pic_huff_create(ctypes.byref(desc), ctypes.byref(h)) == D.PIC_E_NODEVICE
