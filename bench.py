@@ -180,44 +180,98 @@ def zpr_cpu_baseline(wl, stream, target_s=12.0):
                       f"{bpi} blocks) by the fp64 C oracle (OpenMP over blocks), {dt:.1f} s"}
 
 
-def zpr_bench(args, pipeline=False):
-    """Latent decoding from the ZpR symbol stream (``--zpr``), or that step
-    followed by the synthesis in one timed step (``--pipeline``)."""
+def huff_cpu_baseline(hs, wl, target_s=12.0):
+    """The oracle's Huffman decoding of the workload's whole stream, repeated
+    until about target_s seconds of CPU work (it is single-threaded)."""
+    import oracle
+    orc = oracle.default()
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        orc.huffman_decode(hs.data, hs.n_bits, hs.values, hs.lengths, hs.n_symbols)
+        n += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(n * wl.batch * wl.height * wl.width / dt / 1e6, 3), "unit": "Mpixel/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{n} decodes of the workload's {hs.n_bits}-bit stream ({hs.n_symbols} symbols) by the "
+                      f"C oracle (one thread), {dt:.1f} s"}
+
+
+STAGE_NAMES = {
+    ("huff",): "PIC entropy decoding (Huffman bitstream -> ZpR symbols)",
+    ("zpr",): "PIC latent decoding (ZpR symbol stream -> latent pyramid)",
+    ("zpr", "synth"): "PIC decode without entropy decoding (ZpR stream -> latents -> RGB)",
+    ("huff", "zpr", "synth"): "PIC full decode (Huffman bitstream -> ZpR symbols -> latents -> RGB)",
+}
+STAGE_KERNELS = {"huff": "k_huff_table + k_huff_parse + k_huff_check + k_huff_fix + k_huff_count + k_huff_write",
+                 "zpr": "k_zpr_count + k_zpr_expand", "synth": "pic_decode_run"}
+
+
+def stage_bench(args, stages):
+    """Time the decoder stages before (and with) the synthesis, each step
+    running `stages` in order on device-resident inputs:
+      huff   Huffman bitstream -> ZpR symbols   (pic_huff_decode)
+      zpr    ZpR symbols -> latent pyramid      (pic_zpr_decode)
+      synth  latent pyramid -> RGB              (pic_decode_run)"""
     import ctypes
     import numpy as np
     import torch
     from paper_2609_09020_amd import synth
     from paper_2609_09020_amd import decoder as D
+    stages = tuple(stages)
     wl = synth.WORKLOADS[args.workload]
     zs = synth.workload_zpr_stream(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
-    sym = torch.from_numpy(zs.symbols).to(dev)
-    z = D.ZprDecoder(wl.height, wl.width, wl.levels, wl.batch)
-    lat = [torch.empty((wl.batch,) + z.level_shape(k), dtype=torch.float32, device=dev)
-           for k in range(wl.levels)]
-    st = torch.zeros(1, dtype=torch.int32, device=dev)
     lib = D.load_library()
-    lat_arr = (ctypes.c_void_p * wl.levels)(*[t.data_ptr() for t in lat])
-    zargs = (ctypes.c_void_p(z.handle), ctypes.c_int32(wl.batch), ctypes.c_void_p(sym.data_ptr()),
-             ctypes.c_int64(zs.symbols.size), ctypes.c_int32(zs.eob), lat_arr,
-             ctypes.c_void_p(st.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
-    calls = [(lib.pic_zpr_decode, zargs)]
+    sv = ctypes.c_void_p(stream.cuda_stream)
+    calls, handles, checks = [], [], []
+    sym = torch.from_numpy(zs.symbols).to(dev)
+    hs = None
+    if "huff" in stages:
+        hs = synth.make_huff_stream(zs.symbols)
+        hdata = torch.from_numpy(hs.data).to(dev)
+        hvals = torch.from_numpy(hs.values).to(dev)
+        hlens = torch.from_numpy(hs.lengths).to(dev)
+        hst = torch.zeros(1, dtype=torch.int32, device=dev)
+        hd = D.HuffDecoder(hs.n_bits)
+        handles.append(hd)
+        sym = torch.empty(hs.n_symbols, dtype=torch.int32, device=dev)
+        calls.append((lib.pic_huff_decode, (ctypes.c_void_p(hd.handle), ctypes.c_void_p(hdata.data_ptr()),
+                                            ctypes.c_int64(hs.n_bits), ctypes.c_void_p(hvals.data_ptr()),
+                                            ctypes.c_void_p(hlens.data_ptr()), ctypes.c_int32(hs.values.size),
+                                            ctypes.c_int64(hs.n_symbols), ctypes.c_void_p(sym.data_ptr()),
+                                            ctypes.c_void_p(hst.data_ptr()), sv)))
+        checks.append(("entropy decoding", hst))
+    lat_arr = None
+    if "zpr" in stages:
+        z = D.ZprDecoder(wl.height, wl.width, wl.levels, wl.batch)
+        handles.append(z)
+        lat = [torch.empty((wl.batch,) + z.level_shape(k), dtype=torch.float32, device=dev)
+               for k in range(wl.levels)]
+        zst = torch.zeros(1, dtype=torch.int32, device=dev)
+        lat_arr = (ctypes.c_void_p * wl.levels)(*[t.data_ptr() for t in lat])
+        calls.append((lib.pic_zpr_decode, (ctypes.c_void_p(z.handle), ctypes.c_int32(wl.batch),
+                                           ctypes.c_void_p(sym.data_ptr()), ctypes.c_int64(zs.symbols.size),
+                                           ctypes.c_int32(zs.eob), lat_arr, ctypes.c_void_p(zst.data_ptr()), sv)))
+        checks.append(("latent decoding", zst))
     dec = None
-    if pipeline:
+    if "synth" in stages:
         inp = synth.workload_inputs(wl)
         w = torch.from_numpy(inp.weights_bf16.view(np.int16) if inp.weights_bf16 is not None
                              else inp.weights).to(dev)
         b = torch.from_numpy(inp.biases).to(dev)
         dec = D.Decoder(wl.height, wl.width, wl.widths, weight_dtype=wl.weight_dtype,
                         out_dtype=args.out_dtype, max_batch=wl.batch, variant=args.variant)
+        handles.append(dec)
         out = dec.alloc_out(wl.batch, dev)
         calls.append((lib.pic_decode_run,
                       (ctypes.c_void_p(dec.handle), ctypes.c_int32(wl.batch), lat_arr,
                        ctypes.c_void_p(w.data_ptr()), ctypes.c_int64(dec.nw), ctypes.c_void_p(b.data_ptr()),
-                       ctypes.c_int64(dec.nb), ctypes.c_void_p(out.data_ptr()),
-                       ctypes.c_void_p(stream.cuda_stream))))
+                       ctypes.c_int64(dec.nb), ctypes.c_void_p(out.data_ptr()), sv)))
 
     def step():
         for fn, a in calls:
@@ -227,45 +281,79 @@ def zpr_bench(args, pipeline=False):
 
     step()
     torch.cuda.synchronize()
-    if int(st.item()) != 0:
-        raise RuntimeError(f"latent decoding reported status {int(st.item())} on the benchmark stream")
+    for what, st in checks:
+        if int(st.item()) != 0:
+            raise RuntimeError(f"{what} reported status {int(st.item())} on the benchmark stream")
     ms, wall = time_calls(step, args.steps, args.warmup, stream)
+    # latency mode (the paper's serial protocol): synchronise, decode, synchronise
+    lat_n = min(200, max(20, args.steps // 10))
+    tl = 0.0
+    for _ in range(lat_n):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        step()
+        torch.cuda.synchronize()
+        tl += time.perf_counter() - t1
     px = wl.batch * wl.height * wl.width
-    nbytes = zpr_bytes_per_call(wl, zs.symbols.size)
-    name = "k_zpr_count + k_zpr_expand"
     res = {
-        "metric": ("PIC decode without entropy decoding (ZpR stream -> latents -> RGB)" if pipeline
-                   else "PIC latent decoding (ZpR symbol stream -> latent pyramid)"),
-        "value": round(px * args.steps / wall / 1e6, 2), "unit": "Mpixel/s",
+        "metric": STAGE_NAMES[stages], "value": round(px * args.steps / wall / 1e6, 2), "unit": "Mpixel/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(1e3 * wall / args.steps, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "fps": round(wl.batch * args.steps / wall, 1), "kernel_avg_ms": round(ms, 5),
+        "latency_ms": round(1e3 * tl / lat_n, 4),
         "config": {"workload": f"{wl.name}: {wl.note}", "height": wl.height, "width": wl.width,
                    "levels": wl.levels, "batch": wl.batch, "symbols": int(zs.symbols.size),
-                   "blocks": int(zs.blocks), "eob": int(zs.eob), "kernels": name,
-                   "parallelism": "single GPU"},
+                   "blocks": int(zs.blocks), "eob": int(zs.eob),
+                   "kernels": " ; ".join(STAGE_KERNELS[s] for s in stages), "parallelism": "single GPU"},
     }
-    if not pipeline:
-        achieved = nbytes / (ms * 1e-3) / 1e9
-        traffic = load_traffic("k_zpr", args.workload, "latents")
-        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                           "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                           "bytes_per_launch": nbytes, "kernels": name}
-        if not args.no_cpu_baseline:
-            res["cpu_baseline"] = zpr_cpu_baseline(wl, zs)
-    else:
+    if hs is not None:
+        res["config"].update({"bitstream_bits": hs.n_bits, "table_entries": int(hs.values.size),
+                              "longest_code": int(hs.lengths.max())})
+    if dec is not None:
         res["config"].update({"widths": list(wl.widths), "weights": wl.weight_dtype,
                               "out_dtype": args.out_dtype, "synthesis_kernel": dec.info()["kernel_name"]})
+    if stages == ("zpr",):
+        nbytes = zpr_bytes_per_call(wl, zs.symbols.size)
+        achieved = nbytes / (ms * 1e-3) / 1e9
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                           "traffic": load_traffic("k_zpr", args.workload, "latents"),
+                           "bytes_per_launch": nbytes, "kernels": STAGE_KERNELS["zpr"]}
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = zpr_cpu_baseline(wl, zs)
+    if stages == ("huff",):
+        nbytes = (hs.n_bits + 7) // 8 + 4 * hs.n_symbols
+        achieved = nbytes / (ms * 1e-3) / 1e9
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                           "bytes_per_launch": nbytes, "kernels": STAGE_KERNELS["huff"],
+                           "note": "the bitstream read once and the symbols written once; the step is "
+                                   "bound by its serial codeword chains and launch count, not by HBM"}
+        res["symbols_per_s"] = round(hs.n_symbols / (ms * 1e-3), 1)
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = huff_cpu_baseline(hs, wl)
+    if stages == ("huff", "zpr", "synth"):
+        # the same step with the bitstream copied in from pinned host memory
+        # first (context for the paper's per-image figure; not the value)
+        host = torch.from_numpy(hs.data).pin_memory()
+        tl = 0.0
+        for _ in range(lat_n):
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            hdata.copy_(host, non_blocking=True)
+            step()
+            torch.cuda.synchronize()
+            tl += time.perf_counter() - t1
+        res["latency_ms_with_h2d"] = round(1e3 * tl / lat_n, 4)
     if args.copy_calib:
         src = torch.full((256 << 20,), 7, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         for _ in range(5):
             dst.copy_(src)
         torch.cuda.synchronize()
-    z.close()
-    if dec is not None:
-        dec.close()
+    for h in handles:
+        h.close()
     print(json.dumps(res), flush=True)
 
 
@@ -288,6 +376,10 @@ def main():
                          "stream (pic_zpr_decode) on the workload's pyramid shape")
     ap.add_argument("--pipeline", action="store_true",
                     help="time the latent decoding followed by the synthesis as one step")
+    ap.add_argument("--huff", action="store_true",
+                    help="time the Huffman entropy decoding (pic_huff_decode) of the workload's stream")
+    ap.add_argument("--full", action="store_true",
+                    help="time the whole decoder as one step: Huffman bitstream -> symbols -> latents -> RGB")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -304,9 +396,11 @@ def main():
     if args.width_sweep:
         width_sweep(args)
         return
-    if args.zpr or args.pipeline:
-        zpr_bench(args, pipeline=args.pipeline)
-        return
+    for flag, stages in ((args.full, ("huff", "zpr", "synth")), (args.pipeline, ("zpr", "synth")),
+                         (args.huff, ("huff",)), (args.zpr, ("zpr",))):
+        if flag:
+            stage_bench(args, stages)
+            return
 
     wl = synth.WORKLOADS[args.workload]
     inp = synth.workload_inputs(wl)

@@ -7,23 +7,26 @@
 // thread cannot know where the first codeword of its subsequence starts, so
 // it parses from the subsequence's first bit anyway; a parse that starts
 // inside a codeword soon falls onto a true codeword boundary, and from there
-// on it equals the true parse.  Six kernels:
+// on it equals the true parse.  Four kernels:
 //
 //   k_huff_table  (one workgroup) checks the table and builds the canonical
 //                 decode tables: a 2^11-entry first-level table (codes of up
 //                 to 11 bits), per length the first code, the count and the
 //                 first index (longer codes), and the values in code order.
-//   k_huff_parse  parses every subsequence from its first bit (LUT and the
-//                 workgroup's slice of the bitstream in LDS) and records a
-//                 128-bit mask of the codeword starts it visited and where the
-//                 parse crossed into the next subsequence.
-//   k_huff_check  subsequence t is in step if the parse of t - 1 crossed into
-//                 it at a position t's own parse visited; the others are
-//                 recorded in a bitmap.
-//   k_huff_fix    (one workgroup, usually nothing to do) re-parses each
-//                 subsequence that was not in step from the true start, in
-//                 stream order, until its successor is in step again.
-//   k_huff_count  counts each subsequence's codewords from its true start.
+//   k_huff_parse  parses every subsequence from its first bit (tables and the
+//                 workgroup's slice of the bitstream in LDS), then walks from
+//                 where the previous subsequence's parse crossed into it until
+//                 the walk meets its own parse: from there on the two agree,
+//                 so the walk's codeword starts replace the parse's before
+//                 that point.  A workgroup owns 255 subsequences; its first
+//                 thread re-parses the previous workgroup's last one, so the
+//                 whole check stays inside the workgroup.  A walk that does
+//                 not meet the parse before the subsequence ends is recorded.
+//   k_huff_fix    (one workgroup, usually nothing to do) repeats the walk for
+//                 the recorded subsequences in stream order, from the true
+//                 crossing point, carrying a changed crossing point on to the
+//                 next subsequence; finds the first pattern that is no
+//                 codeword; adjusts the counts.
 //   k_huff_write  places each subsequence's symbols by a prefix of the counts
 //                 and decodes them again, writing the values.
 #include "pic_huff.h"
@@ -38,14 +41,14 @@ constexpr int kBlockWords = kHuffThreads * kHuffSub / 32;     // bitstream words
 constexpr int kStageWords = kBlockWords + 2;                  // plus the codeword crossing the end
 constexpr int kTabFirst = 8, kTabCount = 40, kTabIndex = 72;
 
-// Big-endian 32-bit word w of the bitstream (bytes past the end read as 0).
+// Big-endian 32-bit word w of the bitstream (bytes outside it read as 0).
 __device__ __forceinline__ uint32_t stream_word(const uint8_t *data, int32_t n_bytes, int64_t w)
 {
     uint32_t v = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int64_t i = w * 4 + k;
-        v = (v << 8) | (i < n_bytes ? (uint32_t)data[i] : 0u);
+        v = (v << 8) | (i >= 0 && i < n_bytes ? (uint32_t)data[i] : 0u);
     }
     return v;
 }
@@ -223,199 +226,108 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_table(HuffParams p)
         p.lut[i] = s_lut[i];
 }
 
-__global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
+// The 32 bits from absolute bit position `pos`: from the workgroup's staged
+// words (LdsBits) or straight from the bitstream (GlobalBits).
+struct LdsBits {
+    const uint32_t *words;
+    int32_t base;                     // bit position of words[0]
+    __device__ __forceinline__ uint32_t operator()(int32_t pos) const { return window32(words, pos - base); }
+};
+
+struct GlobalBits {
+    const uint8_t *data;
+    int32_t n_bytes;
+    __device__ __forceinline__ uint32_t operator()(int32_t pos) const
+    {
+        return window32_global(data, n_bytes, pos);
+    }
+};
+
+// 128 bits, one per bit offset of a subsequence.
+struct Mask {
+    uint64_t lo, hi;
+};
+
+__device__ __forceinline__ bool mask_has(const Mask &m, int off)
 {
-    __shared__ SharedTables s_tab;
-    __shared__ uint32_t s_words[kStageWords];
-    const int64_t w0 = (int64_t)blockIdx.x * kBlockWords;
-    load_tables(p, s_tab);
-    stage_words(p, s_words, w0);
-    __syncthreads();
-    if (!s_tab.valid)
-        return;
-    const Tables tab = tables_of(s_tab);
-    const int t = blockIdx.x * kHuffThreads + threadIdx.x;
-    if (t >= p.nsub)
-        return;
-    const int32_t start = t * kHuffSub;
-    const int32_t lim = start + kHuffSub < p.n_bits ? start + kHuffSub : p.n_bits;
-    const int32_t local0 = (int32_t)(start - w0 * 32);
-    uint32_t m[4] = {0u, 0u, 0u, 0u};
-    int32_t pos = start, end;
-    while (true) {
-        if (pos >= lim) {
-            end = pos;
+    return ((off < 64 ? m.lo : m.hi) >> (off & 63)) & 1u;
+}
+
+__device__ __forceinline__ void mask_set(Mask &m, int off)
+{
+    const uint64_t bit = 1ull << (off & 63);
+    if (off < 64)
+        m.lo |= bit;
+    else
+        m.hi |= bit;
+}
+
+// The bits of `m` at offsets >= off (0 <= off <= 128).
+__device__ __forceinline__ Mask mask_from(const Mask &m, int off)
+{
+    const uint64_t keep = ~0ull << (off & 63);
+    Mask r;
+    r.lo = off >= 64 ? 0ull : m.lo & keep;
+    r.hi = off >= 128 ? 0ull : off < 64 ? m.hi : m.hi & keep;
+    return r;
+}
+
+__device__ __forceinline__ int mask_count(const Mask &m) { return __popcll(m.lo) + __popcll(m.hi); }
+
+__device__ __forceinline__ Mask load_mask(const HuffParams &p, int t)
+{
+    const uint4 v = reinterpret_cast<const uint4 *>(p.mask)[t];
+    return Mask{(uint64_t)v.y << 32 | v.x, (uint64_t)v.w << 32 | v.z};
+}
+
+__device__ __forceinline__ void store_mask(const HuffParams &p, int t, const Mask &m)
+{
+    reinterpret_cast<uint4 *>(p.mask)[t] =
+        make_uint4((uint32_t)m.lo, (uint32_t)(m.lo >> 32), (uint32_t)m.hi, (uint32_t)(m.hi >> 32));
+}
+
+// How a walk ends.
+enum { kReached = 0, kMet = 1, kInvalid = 2, kPastEnd = 3 };
+
+// Parse from bit *pos of the subsequence that starts at bit `start` and ends
+// before `lim`, setting each codeword start in `m`; with MEET, stop at the
+// first position that `old` holds already.  *pos receives where the walk
+// stopped.
+template <bool MEET, class Bits>
+__device__ __forceinline__ int walk(const Bits &bits, const Tables &tab, int32_t start, int32_t lim,
+                                    int32_t n_bits, const Mask &old, Mask &m, int32_t *pos_io)
+{
+    int32_t pos = *pos_io;
+    int state = kReached;
+    while (pos < lim) {
+        const int off = pos - start;
+        if (MEET && mask_has(old, off)) {
+            state = kMet;
             break;
         }
         int idx;
-        const int len = decode_one(window32(s_words, local0 + (pos - start)), tab, &idx);
+        const int len = decode_one(bits(pos), tab, &idx);
         if (len == 0) {
-            end = -1;                 // no codeword starts here
+            state = kInvalid;
             break;
         }
-        if (pos + len > p.n_bits) {   // the codeword would run past the stream
-            end = p.n_bits;
+        if (len > n_bits - pos) {
+            state = kPastEnd;
             break;
         }
-        const int off = pos - start;
-        m[off >> 5] |= 1u << (off & 31);
+        mask_set(m, off);
         pos += len;
     }
-    reinterpret_cast<uint4 *>(p.mask)[t] = make_uint4(m[0], m[1], m[2], m[3]);
-    p.end[t] = end;
+    *pos_io = pos;
+    return state;
 }
 
-// Is subsequence t in step: did the previous parse cross into it at a
-// codeword start of its own parse?
-__device__ __forceinline__ bool in_step(const HuffParams &p, int t, int32_t b)
+// Where a parse that stopped in `state` at `pos` crosses into the next
+// subsequence: pos itself; -1 after a pattern that is no codeword; n_bits when
+// a codeword would run past the stream.
+__device__ __forceinline__ int32_t crossing(int state, int32_t pos, int32_t n_bits)
 {
-    if (t == 0)
-        return true;
-    if (b < 0)
-        return false;                 // the previous parse met a pattern that is no codeword
-    if (b >= p.n_bits)
-        return true;                  // nothing left of the stream here
-    const uint4 mk = reinterpret_cast<const uint4 *>(p.mask)[t];
-    const int off = b - t * kHuffSub;
-    const uint32_t word = off < 32 ? mk.x : off < 64 ? mk.y : off < 96 ? mk.z : mk.w;
-    return (word >> (off & 31)) & 1u;
-}
-
-__global__ __launch_bounds__(kHuffThreads) void k_huff_check(HuffParams p)
-{
-    __shared__ int32_t s_valid;
-    if (threadIdx.x == 0)
-        s_valid = p.tab[0];
-    __syncthreads();
-    if (!s_valid)
-        return;
-    const int t = blockIdx.x * kHuffThreads + threadIdx.x;
-    bool ok = true;
-    if (t < p.nsub && t > 0)
-        ok = in_step(p, t, p.end[t - 1]);
-    const uint64_t bad = __ballot(!ok);
-    const int lane = threadIdx.x & 63;
-    const int word0 = (blockIdx.x * kHuffThreads + (threadIdx.x & ~63)) >> 5;   // two words per wave
-    if (lane == 0) {
-        p.fail[word0] = (uint32_t)bad;
-        p.fail[word0 + 1] = (uint32_t)(bad >> 32);
-        if (bad)
-            atomicOr(&p.flags[0], 1);
-    }
-}
-
-// Re-parse subsequence t from the true start b (one thread), updating its
-// mask and crossing point.
-__device__ void reparse(const HuffParams &p, const Tables &tab, int t, int32_t b)
-{
-    const int32_t n_bytes = (int32_t)(((int64_t)p.n_bits + 7) >> 3);
-    const int32_t start = t * kHuffSub;
-    const int32_t lim = start + kHuffSub < p.n_bits ? start + kHuffSub : p.n_bits;
-    uint32_t m[4] = {0u, 0u, 0u, 0u};
-    int32_t pos = b, end;
-    while (true) {
-        if (pos >= lim) {
-            end = pos;
-            break;
-        }
-        int idx;
-        const int len = decode_one(window32_global(p.data, n_bytes, pos), tab, &idx);
-        if (len == 0) {
-            end = -1;
-            break;
-        }
-        if (pos + len > p.n_bits) {
-            end = p.n_bits;
-            break;
-        }
-        const int off = pos - start;
-        m[off >> 5] |= 1u << (off & 31);
-        pos += len;
-    }
-    reinterpret_cast<uint4 *>(p.mask)[t] = make_uint4(m[0], m[1], m[2], m[3]);
-    p.end[t] = end;
-}
-
-__global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
-{
-    __shared__ SharedTables s_tab;
-    __shared__ int32_t s_any;
-    __shared__ int32_t s_list[kHuffThreads];
-    __shared__ int32_t s_nlist;
-    if (threadIdx.x == 0)
-        s_any = p.flags[0];
-    load_tables(p, s_tab);
-    __syncthreads();
-    if (!s_any || !s_tab.valid)
-        return;
-    const Tables tab = tables_of(s_tab);
-    const int nwords = ((p.nsub + 63) / 64) * 2;
-    // Walk the bitmap in stream order, a slice of 256 words at a time: the
-    // slice's nonzero words are collected in order, then one thread repairs.
-    for (int base = 0; base < nwords; base += kHuffThreads) {
-        if (threadIdx.x == 0)
-            s_nlist = 0;
-        __syncthreads();
-        const int w = base + threadIdx.x;
-        const uint32_t bits = w < nwords ? p.fail[w] : 0u;
-        const uint64_t nz = __ballot(bits != 0u);
-        __shared__ int32_t s_wn[kWaves];
-        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-        if (lane == 0)
-            s_wn[wave] = __popcll(nz);
-        __syncthreads();
-        int at = __popcll(nz & ((1ull << lane) - 1));
-        for (int k = 0; k < wave; ++k)
-            at += s_wn[k];
-        if (bits)
-            s_list[at] = w;
-        if (threadIdx.x == 0)
-            s_nlist = s_wn[0] + s_wn[1] + s_wn[2] + s_wn[3];
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            for (int k = 0; k < s_nlist; ++k) {
-                const int wd = s_list[k];
-                uint32_t b = p.fail[wd];
-                while (b) {
-                    int t = wd * 32 + __builtin_ctz(b);
-                    b &= b - 1u;
-                    // repair t, then its successors while they are out of step
-                    while (t < p.nsub && !in_step(p, t, p.end[t - 1])) {
-                        const int32_t from = p.end[t - 1];
-                        if (from < 0)
-                            break;            // a pattern that is no codeword upstream: corrupt stream
-                        reparse(p, tab, t, from);
-                        ++t;
-                    }
-                }
-            }
-        }
-        __syncthreads();
-    }
-}
-
-// Codewords of subsequence t from its true start (0 if none reaches it).
-__device__ __forceinline__ int32_t count_from_start(const HuffParams &p, int t, int32_t *b_out)
-{
-    const int32_t b = t == 0 ? 0 : p.end[t - 1];
-    *b_out = b;
-    if (b < 0 || b >= p.n_bits)
-        return 0;
-    const uint4 mk = reinterpret_cast<const uint4 *>(p.mask)[t];
-    const int off = b - t * kHuffSub;
-    const uint32_t m[4] = {mk.x, mk.y, mk.z, mk.w};
-    int32_t n = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int lo = k * 32;
-        uint32_t v = m[k];
-        if (off >= lo + 32)
-            v = 0u;
-        else if (off > lo)
-            v &= ~0u << (off - lo);
-        n += __popc(v);
-    }
-    return n;
+    return state == kInvalid ? -1 : state == kPastEnd ? n_bits : pos;
 }
 
 __device__ __forceinline__ int32_t block_sum_incl(int32_t v, int32_t *s_wsum, int32_t *total)
@@ -442,31 +354,201 @@ __device__ __forceinline__ int32_t block_sum_incl(int32_t v, int32_t *s_wsum, in
     return off + incl;
 }
 
-__global__ __launch_bounds__(kHuffThreads) void k_huff_count(HuffParams p)
+__global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
 {
+    __shared__ SharedTables s_tab;
+    __shared__ uint32_t s_words[kStageWords];
+    __shared__ int32_t s_end[kHuffThreads];
     __shared__ int32_t s_wsum[kWaves];
-    __shared__ int32_t s_valid;
-    if (threadIdx.x == 0)
-        s_valid = p.tab[0];
+    const int l = threadIdx.x;
+    const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;           // first owned subsequence
+    const int64_t w0 = ((int64_t)t0 - 1) * (kHuffSub / 32);      // staged from the one before
+    load_tables(p, s_tab);
+    stage_words(p, s_words, w0);
     __syncthreads();
-    if (!s_valid)
-        return;
-    const int t = blockIdx.x * kHuffThreads + threadIdx.x;
-    int32_t n = 0, b = 0;
-    if (t < p.nsub) {
-        n = count_from_start(p, t, &b);
-        // the true parse itself met a pattern that is no codeword: nothing
-        // after it can be decoded (the smallest such subsequence is the true
-        // one; later ones only look so because their start is not true)
-        if (b >= 0 && b < p.n_bits && p.end[t] < 0) {
-            atomicOr(p.status, PIC_HUFF_ERR_CODE);
-            atomicMin(&p.flags[1], t);
+    if (!s_tab.valid)
+        return;   // uniform
+    const Tables tab = tables_of(s_tab);
+    const LdsBits bits{s_words, (int32_t)(w0 * 32)};
+    const int32_t t = t0 + l - 1;
+    const bool live = t >= 0 && t < p.nsub;
+    const int32_t start = t * kHuffSub;
+    const int32_t lim = start + kHuffSub < p.n_bits ? start + kHuffSub : p.n_bits;
+    Mask m{0ull, 0ull};
+    int32_t end = 0;
+    if (live) {
+        int32_t pos = start;
+        const int st = walk<false>(bits, tab, start, lim, p.n_bits, m, m, &pos);
+        end = crossing(st, pos, p.n_bits);
+    }
+    s_end[l] = end;
+    __syncthreads();
+    // Walk from the previous parse's crossing point to the first codeword
+    // start the two parses share; if the previous parse was true, so is this
+    // one from there on, and the walk's starts replace the parse's before it.
+    bool out_of_step = false;
+    int32_t n = 0;
+    if (live && l > 0) {
+        const int32_t b = t == 0 ? 0 : s_end[l - 1];
+        if (b < 0) {
+            out_of_step = true;            // the previous parse met a pattern that is no codeword
+        } else if (b < p.n_bits) {
+            Mask w{0ull, 0ull};
+            int32_t pos = b;
+            const int st = walk<true>(bits, tab, start, lim, p.n_bits, m, w, &pos);
+            if (st == kMet) {
+                const Mask rest = mask_from(m, pos - start);
+                m = Mask{w.lo | rest.lo, w.hi | rest.hi};
+                // a parse that ends in a pattern that is no codeword: the
+                // fix kernel decides, in stream order, where decoding stops
+                out_of_step = end < 0;
+            } else if (st == kReached && pos == end) {
+                m = w;                     // no shared start, but the same crossing point
+            } else {
+                out_of_step = true;
+            }
+            n = mask_count(m);
         }
+        // b >= n_bits: the stream ended before this subsequence; no codewords
+        store_mask(p, t, m);
+        p.end[t] = end;
+        p.cnt[t] = n;
+    }
+    const uint64_t bad = __ballot(out_of_step);
+    const int lane = l & 63, wave = l >> 6;
+    if (lane == 0) {
+        p.fail[blockIdx.x * 8 + wave * 2] = (uint32_t)bad;
+        p.fail[blockIdx.x * 8 + wave * 2 + 1] = (uint32_t)(bad >> 32);
+        if (bad)
+            atomicOr(&p.flags[0], 1);
     }
     int32_t total;
     (void)block_sum_incl(n, s_wsum, &total);
-    if (threadIdx.x == 0)
+    if (l == 0)
         p.blk[blockIdx.x] = total;
+}
+
+// Walk subsequence u again from the true crossing point of its predecessor
+// until it meets its recorded parse, and update its record and count.
+// Returns true when u's crossing point changed (u + 1 must be walked again);
+// *corrupt is set when the true parse meets a pattern that is no codeword.
+__device__ bool refix(const HuffParams &p, const Tables &tab, const GlobalBits &bits, int u, bool *corrupt)
+{
+    *corrupt = false;
+    const int32_t b = u == 0 ? 0 : p.end[u - 1];
+    if (b < 0)
+        return false;                      // cannot happen: the fix stops at the first such pattern
+    const int32_t start = u * kHuffSub;
+    const int32_t lim = start + kHuffSub < p.n_bits ? start + kHuffSub : p.n_bits;
+    bool carry = false;
+    int32_t n = 0;
+    if (b < p.n_bits) {
+        Mask m = load_mask(p, u);
+        const int32_t end = p.end[u];
+        Mask w{0ull, 0ull};
+        int32_t pos = b;
+        const int st = walk<true>(bits, tab, start, lim, p.n_bits, m, w, &pos);
+        if (st == kMet) {
+            const Mask rest = mask_from(m, pos - start);
+            m = Mask{w.lo | rest.lo, w.hi | rest.hi};
+            *corrupt = end < 0;
+        } else {
+            m = w;
+            const int32_t e = crossing(st, pos, p.n_bits);
+            carry = e != end;
+            *corrupt = st == kInvalid;
+            p.end[u] = e;
+        }
+        store_mask(p, u, m);
+        n = mask_count(m);
+    }
+    const int32_t old = p.cnt[u];
+    if (n != old) {
+        p.cnt[u] = n;
+        p.blk[u / kHuffOwn] += n - old;
+    }
+    return carry;
+}
+
+__global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
+{
+    __shared__ SharedTables s_tab;
+    __shared__ int32_t s_any, s_stop;
+    __shared__ int32_t s_list[kHuffThreads];
+    __shared__ int32_t s_wn[kWaves];
+    __shared__ int32_t s_wsum[kWaves];
+    if (threadIdx.x == 0) {
+        s_any = p.flags[0];
+        s_stop = 0;
+    }
+    load_tables(p, s_tab);
+    __syncthreads();
+    if (!s_tab.valid)
+        return;   // uniform
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (s_any) {
+        const Tables tab = tables_of(s_tab);
+        const GlobalBits bits{p.data, (int32_t)(((int64_t)p.n_bits + 7) >> 3)};
+        const int nwords = p.nblk * 8;
+        // Walk the bitmap in stream order, 256 words at a time: the slice's
+        // nonzero words are listed in order, then one thread repairs.
+        for (int base = 0; base < nwords; base += kHuffThreads) {
+            const int wd = base + threadIdx.x;
+            const uint32_t word = wd < nwords ? p.fail[wd] : 0u;
+            const uint64_t nz = __ballot(word != 0u);
+            if (lane == 0)
+                s_wn[wave] = __popcll(nz);
+            __syncthreads();
+            int at = __popcll(nz & ((1ull << lane) - 1));
+            for (int k = 0; k < wave; ++k)
+                at += s_wn[k];
+            if (word)
+                s_list[at] = wd;
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                const int nlist = s_wn[0] + s_wn[1] + s_wn[2] + s_wn[3];
+                for (int k = 0; k < nlist && !s_stop; ++k) {
+                    const int w = s_list[k];
+                    uint32_t bm = p.fail[w];
+                    while (bm && !s_stop) {
+                        const int l = (w & 7) * 32 + __builtin_ctz(bm);
+                        bm &= bm - 1u;
+                        // repair, then carry a changed crossing point onwards
+                        for (int u = (w >> 3) * kHuffOwn + l - 1; u < p.nsub; ++u) {
+                            bool corrupt;
+                            const bool carry = refix(p, tab, bits, u, &corrupt);
+                            if (corrupt) {
+                                atomicOr(p.status, PIC_HUFF_ERR_CODE);
+                                p.flags[1] = u;
+                                s_stop = 1;
+                                break;
+                            }
+                            if (!carry)
+                                break;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            if (s_stop)
+                break;   // uniform
+        }
+    }
+    if (p.blk_is_prefix) {
+        // exclusive prefixes of the per-workgroup counts, a segment per thread
+        const int seg = (p.nblk + kHuffThreads - 1) / kHuffThreads;
+        const int lo = threadIdx.x * seg, hi = lo + seg < p.nblk ? lo + seg : p.nblk;
+        int32_t sum = 0;
+        for (int g = lo; g < hi; ++g)
+            sum += p.blk[g];
+        int32_t total;
+        int32_t run = block_sum_incl(sum, s_wsum, &total) - sum;
+        for (int g = lo; g < hi; ++g) {
+            const int32_t v = p.blk[g];
+            p.blk[g] = run;
+            run += v;
+        }
+    }
 }
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
@@ -475,45 +557,52 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     __shared__ uint32_t s_words[kStageWords];
     __shared__ int32_t s_sorted[kHuffMaxTable];
     __shared__ int32_t s_wsum[kWaves];
-    const int64_t w0 = (int64_t)blockIdx.x * kBlockWords;
+    const int l = threadIdx.x;
+    const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;
+    const int64_t w0 = ((int64_t)t0 - 1) * (kHuffSub / 32);
     load_tables(p, s_tab);
     stage_words(p, s_words, w0);
-    for (int i = threadIdx.x; i < p.n_table; i += kHuffThreads)
+    for (int i = l; i < p.n_table; i += kHuffThreads)
         s_sorted[i] = p.sorted[i];
     __syncthreads();
     if (!s_tab.valid)
-        return;
+        return;   // uniform
     const Tables tab = tables_of(s_tab);
-    // symbols before this block of subsequences: the earlier blocks' counts
-    int32_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int j = threadIdx.x; j < (int)blockIdx.x; j += 8 * kHuffThreads) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            a[u] += j + u * kHuffThreads < (int)blockIdx.x ? p.blk[j + u * kHuffThreads] : 0;
-    }
+    // symbols before this workgroup's subsequences
     int32_t before;
-    (void)block_sum_incl(((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7])), s_wsum, &before);
-    const int t = blockIdx.x * kHuffThreads + threadIdx.x;
-    int32_t n = 0, b = 0;
-    if (t < p.nsub && t <= p.flags[1])
-        n = count_from_start(p, t, &b);
+    if (p.blk_is_prefix) {
+        before = p.blk[blockIdx.x];
+    } else {
+        int32_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int j = l; j < (int)blockIdx.x; j += 8 * kHuffThreads) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                a[u] += j + u * kHuffThreads < (int)blockIdx.x ? p.blk[j + u * kHuffThreads] : 0;
+        }
+        (void)block_sum_incl(((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7])), s_wsum,
+                             &before);
+    }
+    const int32_t t = t0 + l - 1;
+    // subsequences after the first one whose true parse meets a pattern
+    // that is no codeword hold nothing decodable
+    const int32_t n = l > 0 && t < p.nsub && t <= p.flags[1] ? p.cnt[t] : 0;
     int32_t blk_total;
     const int32_t o = before + block_sum_incl(n, s_wsum, &blk_total) - n;
     // too few codewords: the bits ran out (unless a pattern that is no
     // codeword ended the decoding first, already reported)
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0 && (int64_t)before + blk_total < p.n_symbols &&
+    if (blockIdx.x == gridDim.x - 1 && l == 0 && (int64_t)before + blk_total < p.n_symbols &&
         !(*p.status & PIC_HUFF_ERR_CODE))
         atomicOr(p.status, PIC_HUFF_ERR_BITS);
     if (n == 0 || o >= p.n_symbols)
         return;
-    const int32_t local0 = (int32_t)((int64_t)t * kHuffSub - w0 * 32);
-    int32_t pos = b;
+    const LdsBits bits{s_words, (int32_t)(w0 * 32)};
+    int32_t pos = t == 0 ? 0 : p.end[t - 1];
     const int32_t k_end = o + n < p.n_symbols ? n : p.n_symbols - o;
     for (int32_t k = 0; k < k_end; ++k) {
         int idx;
-        const int len = decode_one(window32(s_words, local0 + (pos - t * kHuffSub)), tab, &idx);
+        const int len = decode_one(bits(pos), tab, &idx);
         if (len == 0)
-            break;                    // cannot happen: the count came from this parse
+            break;                         // cannot happen: the count came from this parse
         p.out[o + k] = s_sorted[idx];
         pos += len;
     }
@@ -523,15 +612,13 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
 
 hipError_t launch_huff(const HuffParams &p, hipStream_t s)
 {
-    if (p.nsub < 1)
+    if (p.nsub < 1 || p.nblk != (p.nsub + kHuffOwn - 1) / kHuffOwn)
         return hipErrorInvalidValue;
     const dim3 block(kHuffThreads);
-    const dim3 grid((unsigned)((p.nsub + kHuffThreads - 1) / kHuffThreads));
+    const dim3 grid((unsigned)p.nblk);
     hipLaunchKernelGGL(k_huff_table, dim3(1), block, 0, s, p);
     hipLaunchKernelGGL(k_huff_parse, grid, block, 0, s, p);
-    hipLaunchKernelGGL(k_huff_check, grid, block, 0, s, p);
     hipLaunchKernelGGL(k_huff_fix, dim3(1), block, 0, s, p);
-    hipLaunchKernelGGL(k_huff_count, grid, block, 0, s, p);
     hipLaunchKernelGGL(k_huff_write, grid, block, 0, s, p);
     return hipGetLastError();
 }

@@ -194,6 +194,42 @@ def test_large_stream_sampled(orc):
     assert st == 0 and np.array_equal(got[:hs.n_symbols], hs.symbols)
 
 
+# 2^24 + 1000 byte-long codewords: 1,048,639 subsequences, more workgroups
+# than the write kernel sums by itself, so the fix kernel turns the
+# per-workgroup counts into prefixes
+N_PREFIX = (1 << 24) + 1000
+
+
+def test_many_workgroups_identity_code():
+    # 256 codes of 8 bits: the decoded stream is the byte stream, mapped
+    rng = np.random.default_rng(11)
+    data = rng.integers(0, 256, N_PREFIX, dtype=np.uint8)
+    values = (np.arange(256, dtype=np.int32) * 3 - 100)
+    lengths = np.full(256, 8, np.uint8)
+    _print_case("identity code", N_PREFIX * 8)
+    got, st = _gpu(data, N_PREFIX * 8, values, lengths, N_PREFIX)
+    assert st == 0 and np.array_equal(got[:N_PREFIX], values[data])
+
+
+def test_many_workgroups_bad_pattern_near_the_end():
+    # 255 codes of 8 bits: the byte 0xff starts no codeword; decoding stops
+    # at the one planted near the end (the same construction, small, is
+    # checked against the oracle below)
+    rng = np.random.default_rng(12)
+    for n, k in ((N_PREFIX, N_PREFIX - 5000), (3000, 2100)):
+        data = rng.integers(0, 255, n, dtype=np.uint8)
+        data[k] = 255
+        values = (np.arange(255, dtype=np.int32) * 7 + 1)
+        lengths = np.full(255, 8, np.uint8)
+        _print_case("bad pattern", n * 8, k)
+        got, st = _gpu(data, n * 8, values, lengths, n)
+        assert st == D.PIC_HUFF_ERR_CODE
+        assert np.array_equal(got[:k], values[data[:k]]) and np.all(got[k:n] == FILL)
+        if n < 10000:
+            want, err, used = oracle.default().huffman_decode(data, n * 8, values, lengths, n)
+            assert err == D.PIC_HUFF_ERR_CODE and want.size == k and used == 8 * k
+
+
 def test_reuse_and_batch_of_calls(orc):
     rng = np.random.default_rng(8)
     with pkg.HuffDecoder(1 << 22) as h:
