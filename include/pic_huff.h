@@ -34,9 +34,9 @@ extern "C" {
 #endif
 
 /* Opaque handle: the device it was created on and its device scratch (the
- * decode tables and per-subsequence parse records: about 24 bytes per 128
- * bits of the longest accepted stream).  Runs on one handle must not
- * overlap: enqueue them on one stream, or synchronise between them. */
+ * per-subsequence parse records: about 16 bytes per 64 bits of the longest
+ * accepted stream).  Runs on one handle must not overlap: enqueue them on one
+ * stream, or synchronise between them. */
 typedef struct pic_huff pic_huff;
 
 enum {

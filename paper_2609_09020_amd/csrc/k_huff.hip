@@ -3,32 +3,39 @@
 // parallel decoding after GPUHD, which relies on Huffman codes
 // resynchronising by themselves).
 //
-// The bitstream is cut into subsequences of 128 bits, one thread each.  A
+// The bitstream is cut into subsequences of 64 bits, one thread each.  A
 // thread cannot know where the first codeword of its subsequence starts, so
 // it parses from the subsequence's first bit anyway; a parse that starts
 // inside a codeword soon falls onto a true codeword boundary, and from there
-// on it equals the true parse.  Four kernels:
+// on it equals the true parse.  Three kernels:
 //
-//   k_huff_table  (one workgroup) checks the table and builds the canonical
-//                 decode tables: a 2^11-entry first-level table (codes of up
-//                 to 11 bits), per length the first code, the count and the
-//                 first index (longer codes), and the values in code order.
-//   k_huff_parse  parses every subsequence from its first bit (tables and the
-//                 workgroup's slice of the bitstream in LDS), then walks from
+//   k_huff_parse  parses every subsequence from its first bit, then walks from
 //                 where the previous subsequence's parse crossed into it until
 //                 the walk meets its own parse: from there on the two agree,
 //                 so the walk's codeword starts replace the parse's before
-//                 that point.  A workgroup owns 255 subsequences; its first
-//                 thread re-parses the previous workgroup's last one, so the
-//                 whole check stays inside the workgroup.  A walk that does
-//                 not meet the parse before the subsequence ends is recorded.
-//   k_huff_fix    (one workgroup, usually nothing to do) repeats the walk for
-//                 the recorded subsequences in stream order, from the true
-//                 crossing point, carrying a changed crossing point on to the
-//                 next subsequence; finds the first pattern that is no
-//                 codeword; adjusts the counts.
+//                 that point.  A walk that meets nothing gives a new crossing
+//                 point, and the next subsequence walks again, until none
+//                 moves.  A workgroup owns 255 subsequences; its first thread
+//                 re-parses the previous workgroup's last one, so all of this
+//                 stays inside the workgroup.
+//   k_huff_fix    (one workgroup, usually nothing to repair) writes the status
+//                 and repeats the walk, in stream order and from the true
+//                 crossing point, for what a workgroup could not settle: a
+//                 first subsequence whose predecessor's crossing point moved,
+//                 a pattern that is no codeword, a codeword past the stream's
+//                 end.  It carries a changed crossing point on to the next
+//                 subsequence, finds the first pattern that is no codeword and
+//                 adjusts the counts.
 //   k_huff_write  places each subsequence's symbols by a prefix of the counts
-//                 and decodes them again, writing the values.
+//                 and decodes the codewords its record marks, writing the
+//                 values through LDS.
+//
+// Each workgroup builds the canonical decode tables in LDS from the (value,
+// length) list: a 2^11-entry first-level table for codes of up to 11 bits
+// (with the length of a second codeword when two fit, so that a parse often
+// takes two codewords a step), and for longer codes the left-aligned limits
+// of each length (the codes of one length fill one interval of the code
+// space, shorter lengths first).
 #include "pic_huff.h"
 #include "pic_internal.h"
 
@@ -37,9 +44,12 @@ namespace {
 
 constexpr int kWaves = kHuffThreads / 64;
 constexpr int kLut = 1 << kHuffLutBits;
-constexpr int kBlockWords = kHuffThreads * kHuffSub / 32;     // bitstream words of one workgroup
-constexpr int kStageWords = kBlockWords + 2;                  // plus the codeword crossing the end
-constexpr int kTabFirst = 8, kTabCount = 40, kTabIndex = 72;
+constexpr int kSubWords = kHuffSub / 32;
+constexpr int kStageWords = kHuffThreads * kSubWords + 2;    // the workgroup's words and the codeword
+                                                             // crossing the end
+constexpr int kLong = kHuffMaxLen - kHuffLutBits;            // lengths beyond the first-level table
+constexpr int kWriteLds = 6144;                              // ints: the table's values in code order,
+                                                             // then the workgroup's symbols if they fit
 
 // Big-endian 32-bit word w of the bitstream (bytes outside it read as 0).
 __device__ __forceinline__ uint32_t stream_word(const uint8_t *data, int32_t n_bytes, int64_t w)
@@ -53,144 +63,137 @@ __device__ __forceinline__ uint32_t stream_word(const uint8_t *data, int32_t n_b
     return v;
 }
 
-// The 32 bits from bit position `pos` of a word array (MSB first).
-__device__ __forceinline__ uint32_t window32(const uint32_t *words, int32_t pos)
-{
-    const int i = pos >> 5, o = pos & 31;
-    const uint64_t two = ((uint64_t)words[i] << 32) | words[i + 1];
-    return (uint32_t)((two << o) >> 32);
-}
-
-// The same straight from the bitstream in global memory.
-__device__ __forceinline__ uint32_t window32_global(const uint8_t *data, int32_t n_bytes, int32_t pos)
-{
-    const int64_t i = pos >> 5;
-    const uint64_t two = ((uint64_t)stream_word(data, n_bytes, i) << 32) | stream_word(data, n_bytes, i + 1);
-    return (uint32_t)((two << (pos & 31)) >> 32);
-}
-
-// Decode tables of one workgroup.
-struct Tables {
-    const uint32_t *lut;
-    const int32_t *fc, *cnt, *fi;     // per length: first code, count, first index
-    int max_len;
-};
-
-// Length of the codeword at the top of `win` (0: no codeword) and its index
-// in code order.
-__device__ __forceinline__ int decode_one(uint32_t win, const Tables &t, int *idx)
-{
-    const uint32_t e = t.lut[win >> (32 - kHuffLutBits)];
-    if (e) {
-        *idx = (int)(e & 0xffffu);
-        return (int)(e >> 16);
-    }
-    for (int l = kHuffLutBits + 1; l <= t.max_len; ++l) {
-        const uint32_t d = (win >> (32 - l)) - (uint32_t)t.fc[l];
-        if (d < (uint32_t)t.cnt[l]) {
-            *idx = t.fi[l] + (int)d;
-            return l;
-        }
-    }
-    return 0;
-}
-
-// LDS copies of the decode tables, filled by load_tables.
+// Decode tables of one workgroup (LDS).
 struct SharedTables {
-    uint32_t lut[kLut];
-    int32_t fc[kHuffMaxLen + 1], cnt[kHuffMaxLen + 1], fi[kHuffMaxLen + 1];
-    int32_t valid, max_len;
+    uint32_t lut[kLut];                  // index | length << 16 | length of a second codeword within
+                                         // the slot's bits << 24; 0: a longer code, or none
+    uint32_t lim[kHuffMaxLen + 1];       // end of the codes of length <= l, as 24-bit left-aligned values
+    int32_t fc[kHuffMaxLen + 1];         // first code of length l
+    int32_t fi[kHuffMaxLen + 1];         // code-order index of the first code of length l
+    int32_t d[kHuffMaxLen + 1];          // fi - fc
+    int32_t cnt[kHuffMaxLen + 1];
+    int32_t run[kHuffMaxLen + 1];        // entries of each length ranked so far
+    int32_t wcnt[kWaves][kHuffMaxLen + 1];
+    int32_t valid;
 };
 
-__device__ __forceinline__ void load_tables(const HuffParams &p, SharedTables &s)
+// The length of table entry threadIdx.x (-1 past the table); read before
+// other loads are waited for.
+__device__ __forceinline__ int first_length(const HuffParams &p)
 {
-    for (int i = threadIdx.x; i < kLut; i += kHuffThreads)
-        s.lut[i] = p.lut[i];
-    if (threadIdx.x <= kHuffMaxLen) {
-        s.fc[threadIdx.x] = p.tab[kTabFirst + threadIdx.x];
-        s.cnt[threadIdx.x] = p.tab[kTabCount + threadIdx.x];
-        s.fi[threadIdx.x] = p.tab[kTabIndex + threadIdx.x];
-    }
-    if (threadIdx.x == 0) {
-        s.valid = p.tab[0];
-        s.max_len = p.tab[1];
-    }
+    return (int)threadIdx.x < p.n_table ? (int)p.lengths[threadIdx.x] : -1;
 }
 
-__device__ __forceinline__ Tables tables_of(const SharedTables &s)
+// The length counts, first codes, first indexes and limits of the canonical
+// code (RFC 1951, Sec. 3.2.2), and whether the table is valid: every length
+// in 1 .. kHuffMaxLen and the Kraft sum at most 1.  `len0` is
+// first_length(p).  All threads.
+__device__ void build_code(const HuffParams &p, SharedTables &s, int len0)
 {
-    return Tables{s.lut, s.fc, s.cnt, s.fi, s.max_len};
-}
-
-// Stage the bitstream words [w0, w0 + kStageWords) in LDS.
-__device__ __forceinline__ void stage_words(const HuffParams &p, uint32_t *words, int64_t w0)
-{
-    const int32_t n_bytes = (int32_t)(((int64_t)p.n_bits + 7) >> 3);
-    for (int i = threadIdx.x; i < kStageWords; i += kHuffThreads)
-        words[i] = stream_word(p.data, n_bytes, w0 + i);
-}
-
-__global__ __launch_bounds__(kHuffThreads) void k_huff_table(HuffParams p)
-{
-    __shared__ int32_t s_count[kHuffMaxLen + 1], s_fc[kHuffMaxLen + 1], s_fi[kHuffMaxLen + 1];
-    __shared__ int32_t s_run[kHuffMaxLen + 1];              // entries of each length in earlier tiles
-    __shared__ int32_t s_wcnt[kWaves][kHuffMaxLen + 1];
-    __shared__ uint32_t s_lut[kLut];
-    __shared__ int32_t s_bad;
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int t = threadIdx.x;
     if (t <= kHuffMaxLen) {
-        s_count[t] = 0;
-        s_run[t] = 0;
+        s.cnt[t] = 0;
+        s.run[t] = 0;
     }
     if (t == 0)
-        s_bad = 0;
-    for (int i = t; i < kLut; i += kHuffThreads)
-        s_lut[i] = 0;
+        s.valid = 1;
     __syncthreads();
     for (int i = t; i < p.n_table; i += kHuffThreads) {
-        const int l = p.lengths[i];
+        const int l = i == t ? len0 : p.lengths[i];
         if (l < 1 || l > kHuffMaxLen)
-            s_bad = 1;
+            s.valid = 0;
         else
-            atomicAdd(&s_count[l], 1);
+            atomicAdd(&s.cnt[l], 1);
     }
     __syncthreads();
-    if (t == 0) {
-        // canonical code (RFC 1951, Sec. 3.2.2) and the Kraft sum
-        int64_t kraft = 0;
-        uint32_t code = 0;
-        int32_t idx = 0, max_len = 0;
-        s_count[0] = 0;
-        s_fc[0] = 0;
-        s_fi[0] = 0;
-        for (int l = 1; l <= kHuffMaxLen; ++l) {
-            kraft += (int64_t)s_count[l] << (kHuffMaxLen - l);
-            code = (code + (uint32_t)s_count[l - 1]) << 1;
-            s_fc[l] = (int32_t)code;
-            s_fi[l] = idx;
-            idx += s_count[l];
-            if (s_count[l])
-                max_len = l;
+    if (t < 32) {
+        // lane l holds length l; prefix sums across the lanes give the first
+        // index of each length and the limits (the Kraft sums: the codes of
+        // length l fill [lim[l - 1], lim[l]) of the 24-bit code space, so the
+        // first code of length l is lim[l - 1] >> (24 - l))
+        const int c = t >= 1 && t <= kHuffMaxLen ? s.cnt[t] : 0;
+        // more than 2^l codes of length l over-subscribe the code by
+        // themselves; clamped so the sums stay in 32 bits
+        const uint32_t w = t >= 1 && t <= kHuffMaxLen
+                               ? (uint32_t)min(c, (1 << t) + 1) << (kHuffMaxLen - t) : 0u;
+        int32_t fi = c;
+        uint32_t lim = w;
+#pragma unroll
+        for (int d = 1; d < 32; d <<= 1) {
+            const int32_t a = __shfl_up(fi, d, 32);
+            const uint32_t b = __shfl_up(lim, d, 32);
+            if (t >= d) {
+                fi += a;
+                lim += b;
+            }
         }
-        if (kraft > (1LL << kHuffMaxLen))
-            s_bad = 1;
-        p.tab[0] = !s_bad;
-        p.tab[1] = max_len;
-        *p.status = s_bad ? PIC_HUFF_ERR_TABLE : 0;
-        p.flags[0] = 0;
-        p.flags[1] = 0x7fffffff;      // first subsequence whose true parse meets no codeword
+        fi -= c;                           // exclusive
+        const uint32_t below = __shfl_up(lim, 1, 32);
+        const int32_t fc = t >= 1 ? (int32_t)(below >> (kHuffMaxLen - t)) : 0;
+        if (t <= kHuffMaxLen) {
+            s.fi[t] = fi;
+            s.fc[t] = fc;
+            s.d[t] = fi - fc;
+            s.lim[t] = lim;
+        }
+        if (t == kHuffMaxLen && lim > (1u << kHuffMaxLen))
+            s.valid = 0;
     }
     __syncthreads();
-    if (t <= kHuffMaxLen) {
-        p.tab[kTabFirst + t] = s_fc[t];
-        p.tab[kTabCount + t] = s_count[t];
-        p.tab[kTabIndex + t] = s_fi[t];
-    }
-    if (s_bad)
-        return;   // uniform
+}
 
-    // Rank of each entry among the entries of its length before it (table
-    // order), 256 entries at a time: per wave a ballot per length.
+// The first-level table: slot k holds the code of up to kHuffLutBits bits
+// that the bits k begin with, and the length of the codeword after it when
+// that one ends within the kHuffLutBits bits too.  Needs build_code; all
+// threads.
+__device__ void build_lut(SharedTables &s)
+{
+    constexpr int kPer = kLut / kHuffThreads;
+    uint32_t lim[kHuffLutBits + 1];
+    int32_t fc[kHuffLutBits + 1], fi[kHuffLutBits + 1];
+#pragma unroll
+    for (int l = 1; l <= kHuffLutBits; ++l) {
+        lim[l] = s.lim[l];
+        fc[l] = s.fc[l];
+        fi[l] = s.fi[l];
+    }
+    uint32_t ent[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int k = threadIdx.x + j * kHuffThreads;
+        const uint32_t v = (uint32_t)k << (kHuffMaxLen - kHuffLutBits);
+        uint32_t e = 0;
+#pragma unroll
+        for (int l = kHuffLutBits; l >= 1; --l)
+            if (v < lim[l])
+                e = (uint32_t)(fi[l] + (k >> (kHuffLutBits - l)) - fc[l]) | (uint32_t)l << 16;
+        ent[j] = e;
+        s.lut[k] = e;
+    }
+    __syncthreads();
+    // the bits after the first codeword, padded with zeros, begin the second
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int k = threadIdx.x + j * kHuffThreads;
+        const int len1 = (int)(ent[j] >> 16);
+        if (len1 > 0 && len1 < kHuffLutBits) {
+            const int len2 = (int)(s.lut[(k << len1) & (kLut - 1)] >> 16);
+            if (len2 > 0 && len1 + len2 <= kHuffLutBits)
+                ent[j] |= (uint32_t)len2 << 24;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPer; ++j)
+        s.lut[threadIdx.x + j * kHuffThreads] = ent[j];
+    __syncthreads();
+}
+
+// The table's values in code order (by length, then table order).  Needs
+// build_code; all threads.
+__device__ void build_sorted(const HuffParams &p, SharedTables &s, int32_t *sorted)
+{
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     for (int base = 0; base < p.n_table; base += kHuffThreads) {
         const int i = base + t;
         const int l = i < p.n_table ? p.lengths[i] : 0;
@@ -200,90 +203,126 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_table(HuffParams p)
             if (l == k)
                 in_wave = __popcll(m & ((1ull << lane) - 1));
             if (lane == 0)
-                s_wcnt[wave][k] = __popcll(m);
+                s.wcnt[wave][k] = __popcll(m);
         }
         __syncthreads();
         if (l > 0) {
-            int rank = s_run[l] + in_wave;
+            int rank = s.run[l] + in_wave;
             for (int w = 0; w < wave; ++w)
-                rank += s_wcnt[w][l];
-            const int si = s_fi[l] + rank;
-            const uint32_t code = (uint32_t)s_fc[l] + (uint32_t)rank;
-            p.sorted[si] = p.values[i];
-            if (l <= kHuffLutBits) {
-                const uint32_t first = code << (kHuffLutBits - l), n = 1u << (kHuffLutBits - l);
-                for (uint32_t k = 0; k < n; ++k)
-                    s_lut[first + k] = (uint32_t)si | (uint32_t)l << 16;
-            }
+                rank += s.wcnt[w][l];
+            sorted[s.fi[l] + rank] = p.values[i];
         }
         __syncthreads();
         if (t >= 1 && t <= kHuffMaxLen)
             for (int w = 0; w < kWaves; ++w)
-                s_run[t] += s_wcnt[w][t];
+                s.run[t] += s.wcnt[w][t];
         __syncthreads();
     }
-    for (int i = t; i < kLut; i += kHuffThreads)
-        p.lut[i] = s_lut[i];
 }
 
-// The 32 bits from absolute bit position `pos`: from the workgroup's staged
-// words (LdsBits) or straight from the bitstream (GlobalBits).
-struct LdsBits {
-    const uint32_t *words;
-    int32_t base;                     // bit position of words[0]
-    __device__ __forceinline__ uint32_t operator()(int32_t pos) const { return window32(words, pos - base); }
+// Per-thread view of the tables: the limits of the long lengths in registers.
+struct Decoder {
+    const uint32_t *lut;
+    const int32_t *d;
+    uint32_t lim[kLong];                 // lim[j]: limit of length kHuffLutBits + 1 + j; lim[kLong - 1]
+                                         // (length kHuffMaxLen) is the end of the whole code
 };
 
-struct GlobalBits {
-    const uint8_t *data;
-    int32_t n_bytes;
-    __device__ __forceinline__ uint32_t operator()(int32_t pos) const
+__device__ __forceinline__ Decoder decoder_of(const SharedTables &s)
+{
+    Decoder dc;
+    dc.lut = s.lut;
+    dc.d = s.d;
+#pragma unroll
+    for (int j = 0; j < kLong; ++j)
+        dc.lim[j] = s.lim[kHuffLutBits + 1 + j];
+    return dc;
+}
+
+// Length of a codeword longer than the first-level table at the top of
+// `win` (0: no codeword starts there).
+__device__ __forceinline__ int decode_long(uint32_t win, const Decoder &dc)
+{
+    const uint32_t v = win >> (32 - kHuffMaxLen);
+    if (v >= dc.lim[kLong - 1])
+        return 0;                        // past the last code: no codeword has these bits
+    // the length whose interval holds v: one past the lengths whose limit is <= v
+    int len = kHuffLutBits + 1;
+#pragma unroll
+    for (int j = 0; j < kLong - 1; ++j)
+        len += v >= dc.lim[j] ? 1 : 0;
+    return len;
+}
+
+// Length of the codeword at the top of `win` (0: no codeword starts there)
+// and its index in code order.
+__device__ __forceinline__ int decode_one(uint32_t win, const Decoder &dc, int *idx)
+{
+    const uint32_t e = dc.lut[win >> (32 - kHuffLutBits)];
+    if (e) {
+        *idx = (int)(e & 0xfffu);
+        return (int)((e >> 16) & 0xffu);
+    }
+    const int len = decode_long(win, dc);
+    *idx = len ? (int)(win >> (32 - len)) + dc.d[len] : 0;
+    return len;
+}
+
+// Stage the bitstream words [w0, w0 + kStageWords) in LDS (every load issued
+// before the first is waited for).
+__device__ __forceinline__ void stage_words(const HuffParams &p, uint32_t *words, int64_t w0)
+{
+    constexpr int kPer = (kStageWords + kHuffThreads - 1) / kHuffThreads;
+    const int32_t n_bytes = (int32_t)(((int64_t)p.n_bits + 7) >> 3);
+    uint32_t v[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = threadIdx.x + j * kHuffThreads;
+        v[j] = i < kStageWords ? stream_word(p.data, n_bytes, w0 + i) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = threadIdx.x + j * kHuffThreads;
+        if (i < kStageWords)
+            words[i] = v[j];
+    }
+}
+
+// The bits of one subsequence (two words) and the word after it.
+struct SubBits {
+    uint32_t w0, w1, w2;
+    // the 32 bits from bit offset `off` of the subsequence (0 <= off < 64)
+    __device__ __forceinline__ uint32_t window(int off) const
     {
-        return window32_global(data, n_bytes, pos);
+        const uint64_t two = off < 32 ? (uint64_t)w0 << 32 | w1 : (uint64_t)w1 << 32 | w2;
+        return (uint32_t)(two << (off & 31) >> 32);
     }
 };
 
-// 128 bits, one per bit offset of a subsequence.
-struct Mask {
-    uint64_t lo, hi;
-};
+static_assert(kSubWords == 2, "a subsequence is two words");
 
-__device__ __forceinline__ bool mask_has(const Mask &m, int off)
+// From the workgroup's staged words, starting at word `first`.
+__device__ __forceinline__ SubBits lds_sub(const uint32_t *words, int first)
 {
-    return ((off < 64 ? m.lo : m.hi) >> (off & 63)) & 1u;
+    return SubBits{words[first], words[first + 1], words[first + 2]};
 }
 
-__device__ __forceinline__ void mask_set(Mask &m, int off)
+// Subsequence `t` straight from the bitstream.
+__device__ __forceinline__ SubBits global_sub(const HuffParams &p, int t)
 {
-    const uint64_t bit = 1ull << (off & 63);
-    if (off < 64)
-        m.lo |= bit;
-    else
-        m.hi |= bit;
+    const int32_t n_bytes = (int32_t)(((int64_t)p.n_bits + 7) >> 3);
+    const int64_t w = (int64_t)t * kSubWords;
+    return SubBits{stream_word(p.data, n_bytes, w), stream_word(p.data, n_bytes, w + 1),
+                   stream_word(p.data, n_bytes, w + 2)};
 }
 
-// The bits of `m` at offsets >= off (0 <= off <= 128).
-__device__ __forceinline__ Mask mask_from(const Mask &m, int off)
-{
-    const uint64_t keep = ~0ull << (off & 63);
-    Mask r;
-    r.lo = off >= 64 ? 0ull : m.lo & keep;
-    r.hi = off >= 128 ? 0ull : off < 64 ? m.hi : m.hi & keep;
-    return r;
-}
+// A record of codeword starts: bit k for bit offset k of a subsequence.
+__device__ __forceinline__ bool mask_has(uint64_t m, int off) { return (m >> (off & 63)) & 1u; }
 
-__device__ __forceinline__ int mask_count(const Mask &m) { return __popcll(m.lo) + __popcll(m.hi); }
-
-__device__ __forceinline__ Mask load_mask(const HuffParams &p, int t)
+// The bits of `m` at offsets >= off (0 <= off <= 64).
+__device__ __forceinline__ uint64_t mask_from(uint64_t m, int off)
 {
-    const uint4 v = reinterpret_cast<const uint4 *>(p.mask)[t];
-    return Mask{(uint64_t)v.y << 32 | v.x, (uint64_t)v.w << 32 | v.z};
-}
-
-__device__ __forceinline__ void store_mask(const HuffParams &p, int t, const Mask &m)
-{
-    reinterpret_cast<uint4 *>(p.mask)[t] =
-        make_uint4((uint32_t)m.lo, (uint32_t)(m.lo >> 32), (uint32_t)m.hi, (uint32_t)(m.hi >> 32));
+    return off >= 64 ? 0ull : m & (~0ull << off);
 }
 
 // How a walk ends.
@@ -293,9 +332,9 @@ enum { kReached = 0, kMet = 1, kInvalid = 2, kPastEnd = 3 };
 // before `lim`, setting each codeword start in `m`; with MEET, stop at the
 // first position that `old` holds already.  *pos receives where the walk
 // stopped.
-template <bool MEET, class Bits>
-__device__ __forceinline__ int walk(const Bits &bits, const Tables &tab, int32_t start, int32_t lim,
-                                    int32_t n_bits, const Mask &old, Mask &m, int32_t *pos_io)
+template <bool MEET>
+__device__ __forceinline__ int walk(const SubBits &bits, const Decoder &dc, int32_t start, int32_t lim,
+                                    int32_t n_bits, uint64_t old, uint64_t &m, int32_t *pos_io)
 {
     int32_t pos = *pos_io;
     int state = kReached;
@@ -305,8 +344,11 @@ __device__ __forceinline__ int walk(const Bits &bits, const Tables &tab, int32_t
             state = kMet;
             break;
         }
-        int idx;
-        const int len = decode_one(bits(pos), tab, &idx);
+        const uint32_t win = bits.window(off);
+        const uint32_t e = dc.lut[win >> (32 - kHuffLutBits)];
+        int len = (int)((e >> 16) & 0xffu);
+        if (len == 0)
+            len = decode_long(win, dc);
         if (len == 0) {
             state = kInvalid;
             break;
@@ -315,8 +357,15 @@ __device__ __forceinline__ int walk(const Bits &bits, const Tables &tab, int32_t
             state = kPastEnd;
             break;
         }
-        mask_set(m, off);
-        pos += len;
+        // the table's second codeword too, when it starts inside the
+        // subsequence, ends inside the stream and (walking to meet `old`)
+        // starts before the meeting point
+        const int len2 = (int)(e >> 24);
+        const int off2 = off + len;
+        const bool two = len2 > 0 && pos + len < lim && len2 <= n_bits - pos - len &&
+                         !(MEET && mask_has(old, off2));
+        m |= 1ull << off | (two ? 1ull << (off2 & 63) : 0ull);
+        pos += two ? len + len2 : len;
     }
     *pos_io = pos;
     return state;
@@ -359,83 +408,111 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
     __shared__ SharedTables s_tab;
     __shared__ uint32_t s_words[kStageWords];
     __shared__ int32_t s_end[kHuffThreads];
+    __shared__ int32_t s_moved[kHuffThreads];
     __shared__ int32_t s_wsum[kWaves];
     const int l = threadIdx.x;
     const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;           // first owned subsequence
-    const int64_t w0 = ((int64_t)t0 - 1) * (kHuffSub / 32);      // staged from the one before
-    load_tables(p, s_tab);
+    const int64_t w0 = ((int64_t)t0 - 1) * kSubWords;            // staged from the one before
+    const int len0 = first_length(p);
     stage_words(p, s_words, w0);
-    __syncthreads();
+    build_code(p, s_tab, len0);
     if (!s_tab.valid)
         return;   // uniform
-    const Tables tab = tables_of(s_tab);
-    const LdsBits bits{s_words, (int32_t)(w0 * 32)};
+    build_lut(s_tab);
+    const Decoder dc = decoder_of(s_tab);
     const int32_t t = t0 + l - 1;
     const bool live = t >= 0 && t < p.nsub;
     const int32_t start = t * kHuffSub;
     const int32_t lim = start + kHuffSub < p.n_bits ? start + kHuffSub : p.n_bits;
-    Mask m{0ull, 0ull};
+    const SubBits bits = lds_sub(s_words, l * kSubWords);
+    uint64_t m = 0;
     int32_t end = 0;
     if (live) {
         int32_t pos = start;
-        const int st = walk<false>(bits, tab, start, lim, p.n_bits, m, m, &pos);
+        const int st = walk<false>(bits, dc, start, lim, p.n_bits, 0ull, m, &pos);
         end = crossing(st, pos, p.n_bits);
     }
+    const int32_t nominal_end = end;
     s_end[l] = end;
     __syncthreads();
-    // Walk from the previous parse's crossing point to the first codeword
-    // start the two parses share; if the previous parse was true, so is this
-    // one from there on, and the walk's starts replace the parse's before it.
-    bool out_of_step = false;
+    // Walk from the previous subsequence's crossing point to the first
+    // codeword start the walk shares with this subsequence's parse; from there
+    // on the two agree, so the walk's starts replace the parse's before it.
+    // A walk that meets nothing ends at a new crossing point, and the next
+    // subsequence walks again, until no crossing point moves.  Subsequences
+    // whose walk meets a pattern that is no codeword, runs past the stream or
+    // follows such a one are left to the fix kernel, which decides in stream
+    // order.
+    bool bad = false, redo = live && l > 0;
     int32_t n = 0;
-    if (live && l > 0) {
-        const int32_t b = t == 0 ? 0 : s_end[l - 1];
-        if (b < 0) {
-            out_of_step = true;            // the previous parse met a pattern that is no codeword
-        } else if (b < p.n_bits) {
-            Mask w{0ull, 0ull};
-            int32_t pos = b;
-            const int st = walk<true>(bits, tab, start, lim, p.n_bits, m, w, &pos);
-            if (st == kMet) {
-                const Mask rest = mask_from(m, pos - start);
-                m = Mask{w.lo | rest.lo, w.hi | rest.hi};
-                // a parse that ends in a pattern that is no codeword: the
-                // fix kernel decides, in stream order, where decoding stops
-                out_of_step = end < 0;
-            } else if (st == kReached && pos == end) {
-                m = w;                     // no shared start, but the same crossing point
+    while (true) {
+        bool moved = false;
+        if (redo) {
+            const int32_t b = t == 0 ? 0 : s_end[l - 1];
+            if (b < 0) {
+                bad = true;
+            } else if (b >= p.n_bits) {
+                n = 0;                     // the stream ended before this subsequence
             } else {
-                out_of_step = true;
+                uint64_t w = 0;
+                int32_t pos = b;
+                const int st = walk<true>(bits, dc, start, lim, p.n_bits, m, w, &pos);
+                if (st == kMet) {
+                    m = w | mask_from(m, pos - start);
+                    bad = end < 0;
+                } else if (st == kReached) {
+                    m = w;
+                    moved = pos != end;
+                    end = pos;
+                } else {
+                    bad = true;
+                }
+                n = __popcll(m);
             }
-            n = mask_count(m);
         }
-        // b >= n_bits: the stream ended before this subsequence; no codewords
-        store_mask(p, t, m);
+        __syncthreads();                   // every read of s_end is done
+        s_end[l] = end;
+        s_moved[l] = moved;
+        if (!__syncthreads_or(moved))
+            break;   // uniform
+        redo = live && l > 0 && !bad && s_moved[l - 1];
+    }
+    // the workgroup's sums first: their barriers then wait for no stores
+    int32_t total;
+    (void)block_sum_incl(n, s_wsum, &total);
+    const bool any_bad = __syncthreads_or(bad);
+    if (live && l > 0) {
+        p.mask[t] = m;
         p.end[t] = end;
         p.cnt[t] = n;
     }
-    const uint64_t bad = __ballot(out_of_step);
+    const uint64_t fail = __ballot(bad);
     const int lane = l & 63, wave = l >> 6;
     if (lane == 0) {
-        p.fail[blockIdx.x * 8 + wave * 2] = (uint32_t)bad;
-        p.fail[blockIdx.x * 8 + wave * 2 + 1] = (uint32_t)(bad >> 32);
-        if (bad)
-            atomicOr(&p.flags[0], 1);
+        p.fail[blockIdx.x * 8 + wave * 2] = (uint32_t)fail;
+        p.fail[blockIdx.x * 8 + wave * 2 + 1] = (uint32_t)(fail >> 32);
     }
-    int32_t total;
-    (void)block_sum_incl(n, s_wsum, &total);
     if (l == 0)
         p.blk[blockIdx.x] = total;
+    // bit 0: the next workgroup took this one's last nominal crossing point,
+    // and it moved; bit 1: a subsequence here was left to the fix kernel
+    if (l == kHuffThreads - 1)
+        p.bnd[blockIdx.x] = (live && end != nominal_end ? 1 : 0) | (any_bad ? 2 : 0);
 }
 
 // Walk subsequence u again from the true crossing point of its predecessor
 // until it meets its recorded parse, and update its record and count.
 // Returns true when u's crossing point changed (u + 1 must be walked again);
 // *corrupt is set when the true parse meets a pattern that is no codeword.
-__device__ bool refix(const HuffParams &p, const Tables &tab, const GlobalBits &bits, int u, bool *corrupt)
+__device__ bool refix(const HuffParams &p, const Decoder &dc, int u, bool *corrupt)
 {
     *corrupt = false;
+    // every load first, in one round trip
     const int32_t b = u == 0 ? 0 : p.end[u - 1];
+    const SubBits bits = global_sub(p, u);
+    uint64_t m = p.mask[u];
+    const int32_t end = p.end[u];
+    const int32_t old = p.cnt[u];
     if (b < 0)
         return false;                      // cannot happen: the fix stops at the first such pattern
     const int32_t start = u * kHuffSub;
@@ -443,14 +520,11 @@ __device__ bool refix(const HuffParams &p, const Tables &tab, const GlobalBits &
     bool carry = false;
     int32_t n = 0;
     if (b < p.n_bits) {
-        Mask m = load_mask(p, u);
-        const int32_t end = p.end[u];
-        Mask w{0ull, 0ull};
+        uint64_t w = 0;
         int32_t pos = b;
-        const int st = walk<true>(bits, tab, start, lim, p.n_bits, m, w, &pos);
+        const int st = walk<true>(bits, dc, start, lim, p.n_bits, m, w, &pos);
         if (st == kMet) {
-            const Mask rest = mask_from(m, pos - start);
-            m = Mask{w.lo | rest.lo, w.hi | rest.hi};
+            m = w | mask_from(m, pos - start);
             *corrupt = end < 0;
         } else {
             m = w;
@@ -459,10 +533,9 @@ __device__ bool refix(const HuffParams &p, const Tables &tab, const GlobalBits &
             *corrupt = st == kInvalid;
             p.end[u] = e;
         }
-        store_mask(p, u, m);
-        n = mask_count(m);
+        p.mask[u] = m;
+        n = __popcll(m);
     }
-    const int32_t old = p.cnt[u];
     if (n != old) {
         p.cnt[u] = n;
         p.blk[u / kHuffOwn] += n - old;
@@ -472,70 +545,93 @@ __device__ bool refix(const HuffParams &p, const Tables &tab, const GlobalBits &
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
 {
+    constexpr int kList = 2048;            // workgroups to repair listed in LDS
     __shared__ SharedTables s_tab;
-    __shared__ int32_t s_any, s_stop;
-    __shared__ int32_t s_list[kHuffThreads];
-    __shared__ int32_t s_wn[kWaves];
+    __shared__ int32_t s_list[kList];
     __shared__ int32_t s_wsum[kWaves];
-    if (threadIdx.x == 0) {
-        s_any = p.flags[0];
-        s_stop = 0;
+    // Workgroups to repair: those that left subsequences to this kernel, and
+    // those whose first subsequence (thread 1) started from a crossing point
+    // that moved in the previous workgroup.  Each thread takes a segment of
+    // workgroups (eight loads in flight at a time) and the workgroup lists
+    // them in stream order; one thread then repairs them.
+    const int nblk = p.nblk;
+    auto needs_fix = [&](int g) { return (p.bnd[g] & 2) || (g > 0 && (p.bnd[g - 1] & 1)); };
+    const int seg = (nblk + kHuffThreads - 1) / kHuffThreads;
+    const int seg_lo = threadIdx.x * seg, seg_hi = seg_lo + seg < nblk ? seg_lo + seg : nblk;
+    const int len0 = first_length(p);
+    int32_t count = 0;
+    uint32_t mine = 0;                     // the segment's workgroups to repair, while seg <= 32
+    for (int g = seg_lo; g < seg_hi; g += 8) {
+        int32_t f[8], b[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            f[j] = g + j < seg_hi ? p.bnd[g + j] & 2 : 0;
+            b[j] = g + j < seg_hi && g + j > 0 ? p.bnd[g + j - 1] & 1 : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (f[j] | b[j]) {
+                ++count;
+                if (g + j - seg_lo < 32)
+                    mine |= 1u << (g + j - seg_lo);
+            }
     }
-    load_tables(p, s_tab);
-    __syncthreads();
+    build_code(p, s_tab, len0);
+    if (threadIdx.x == 0) {
+        *p.status = s_tab.valid ? 0 : PIC_HUFF_ERR_TABLE;
+        p.flags[1] = 0x7fffffff;           // first subsequence whose true parse meets no codeword
+    }
     if (!s_tab.valid)
         return;   // uniform
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (s_any) {
-        const Tables tab = tables_of(s_tab);
-        const GlobalBits bits{p.data, (int32_t)(((int64_t)p.n_bits + 7) >> 3)};
-        const int nwords = p.nblk * 8;
-        // Walk the bitmap in stream order, 256 words at a time: the slice's
-        // nonzero words are listed in order, then one thread repairs.
-        for (int base = 0; base < nwords; base += kHuffThreads) {
-            const int wd = base + threadIdx.x;
-            const uint32_t word = wd < nwords ? p.fail[wd] : 0u;
-            const uint64_t nz = __ballot(word != 0u);
-            if (lane == 0)
-                s_wn[wave] = __popcll(nz);
-            __syncthreads();
-            int at = __popcll(nz & ((1ull << lane) - 1));
-            for (int k = 0; k < wave; ++k)
-                at += s_wn[k];
-            if (word)
-                s_list[at] = wd;
-            __syncthreads();
-            if (threadIdx.x == 0) {
-                const int nlist = s_wn[0] + s_wn[1] + s_wn[2] + s_wn[3];
-                for (int k = 0; k < nlist && !s_stop; ++k) {
-                    const int w = s_list[k];
-                    uint32_t bm = p.fail[w];
-                    while (bm && !s_stop) {
-                        const int l = (w & 7) * 32 + __builtin_ctz(bm);
-                        bm &= bm - 1u;
+    int32_t total;
+    const int32_t at = block_sum_incl(count, s_wsum, &total) - count;
+    if (total > 0) {   // uniform
+        const bool listed = total <= kList && seg <= 32;
+        if (listed)
+            for (uint32_t b = mine; b; b &= b - 1u)
+                s_list[at + __popc(mine & ((1u << __builtin_ctz(b)) - 1u))] = seg_lo + __builtin_ctz(b);
+        build_lut(s_tab);                  // its barriers also publish the list
+        const Decoder dc = decoder_of(s_tab);
+        if (threadIdx.x == 0) {
+            // one workgroup's records, then the chain from each
+            auto repair = [&](int g) -> bool {
+                const uint4 lo = reinterpret_cast<const uint4 *>(p.fail)[g * 2];
+                const uint4 hi = reinterpret_cast<const uint4 *>(p.fail)[g * 2 + 1];
+                const uint32_t words[8] = {lo.x | (g > 0 && (p.bnd[g - 1] & 1) ? 2u : 0u), lo.y, lo.z, lo.w,
+                                           hi.x, hi.y, hi.z, hi.w};
+#pragma unroll 1
+                for (int w = 0; w < 8; ++w)
+                    for (uint32_t bm = words[w]; bm; bm &= bm - 1u) {
+                        const int l = w * 32 + __builtin_ctz(bm);
                         // repair, then carry a changed crossing point onwards
-                        for (int u = (w >> 3) * kHuffOwn + l - 1; u < p.nsub; ++u) {
+                        for (int u = g * kHuffOwn + l - 1; u < p.nsub; ++u) {
                             bool corrupt;
-                            const bool carry = refix(p, tab, bits, u, &corrupt);
+                            const bool carry = refix(p, dc, u, &corrupt);
                             if (corrupt) {
                                 atomicOr(p.status, PIC_HUFF_ERR_CODE);
                                 p.flags[1] = u;
-                                s_stop = 1;
-                                break;
+                                return true;
                             }
                             if (!carry)
                                 break;
                         }
                     }
-                }
+                return false;
+            };
+            if (listed) {
+                for (int k = 0; k < total; ++k)
+                    if (repair(s_list[k]))
+                        break;
+            } else {
+                for (int g = 0; g < nblk; ++g)
+                    if (needs_fix(g) && repair(g))
+                        break;
             }
-            __syncthreads();
-            if (s_stop)
-                break;   // uniform
         }
     }
     if (p.blk_is_prefix) {
         // exclusive prefixes of the per-workgroup counts, a segment per thread
+        __syncthreads();
         const int seg = (p.nblk + kHuffThreads - 1) / kHuffThreads;
         const int lo = threadIdx.x * seg, hi = lo + seg < p.nblk ? lo + seg : p.nblk;
         int32_t sum = 0;
@@ -555,19 +651,20 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
 {
     __shared__ SharedTables s_tab;
     __shared__ uint32_t s_words[kStageWords];
-    __shared__ int32_t s_sorted[kHuffMaxTable];
+    __shared__ int32_t s_vals[kWriteLds];
     __shared__ int32_t s_wsum[kWaves];
+    static_assert(kWriteLds > kHuffMaxTable, "room for the values");
     const int l = threadIdx.x;
     const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;
-    const int64_t w0 = ((int64_t)t0 - 1) * (kHuffSub / 32);
-    load_tables(p, s_tab);
+    const int64_t w0 = ((int64_t)t0 - 1) * kSubWords;
+    const int len0 = first_length(p);
     stage_words(p, s_words, w0);
-    for (int i = l; i < p.n_table; i += kHuffThreads)
-        s_sorted[i] = p.sorted[i];
-    __syncthreads();
+    build_code(p, s_tab, len0);
     if (!s_tab.valid)
         return;   // uniform
-    const Tables tab = tables_of(s_tab);
+    build_lut(s_tab);
+    build_sorted(p, s_tab, s_vals);
+    const Decoder dc = decoder_of(s_tab);
     // symbols before this workgroup's subsequences
     int32_t before;
     if (p.blk_is_prefix) {
@@ -593,18 +690,57 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     if (blockIdx.x == gridDim.x - 1 && l == 0 && (int64_t)before + blk_total < p.n_symbols &&
         !(*p.status & PIC_HUFF_ERR_CODE))
         atomicOr(p.status, PIC_HUFF_ERR_BITS);
-    if (n == 0 || o >= p.n_symbols)
-        return;
-    const LdsBits bits{s_words, (int32_t)(w0 * 32)};
-    int32_t pos = t == 0 ? 0 : p.end[t - 1];
+    // the workgroup's symbols go through LDS when they fit, so that the
+    // stores are contiguous (uniform)
+    const bool staged = blk_total <= kWriteLds - p.n_table;
+    if (n == 0 || o >= p.n_symbols) {
+        if (!staged)
+            return;
+    } else {
+    // the record marks every codeword start of the true parse: the codewords
+    // are decoded independently, four at a time
+    const SubBits bits = lds_sub(s_words, l * kSubWords);
+    uint64_t m = p.mask[t];
     const int32_t k_end = o + n < p.n_symbols ? n : p.n_symbols - o;
-    for (int32_t k = 0; k < k_end; ++k) {
-        int idx;
-        const int len = decode_one(bits(pos), tab, &idx);
-        if (len == 0)
-            break;                         // cannot happen: the count came from this parse
-        p.out[o + k] = s_sorted[idx];
-        pos += len;
+    int32_t *out = staged ? s_vals + p.n_table + (o - before) : p.out + o;
+    for (int32_t k = 0; k < k_end; k += 4) {
+        uint32_t win[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int off = __builtin_ctzll(m | 1ull << 63);   // past the last start: unused
+            m &= m - 1;
+            win[j] = bits.window(off);
+        }
+        // the four table reads first, then the rare long codes, then the
+        // four value reads
+        uint32_t e[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            e[j] = dc.lut[win[j] >> (32 - kHuffLutBits)];
+        int idx[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            idx[j] = (int)(e[j] & 0xfffu);
+            if (e[j] == 0u) {
+                const int len = decode_long(win[j], dc);
+                idx[j] = len ? (int)(win[j] >> (32 - len)) + dc.d[len] : 0;
+            }
+        }
+        int32_t v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            v[j] = s_vals[idx[j]];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (k + j < k_end)
+                out[k + j] = v[j];
+    }
+    }
+    if (staged) {
+        __syncthreads();
+        const int32_t count = before >= p.n_symbols ? 0 : min(blk_total, p.n_symbols - before);
+        for (int32_t i = l; i < count; i += kHuffThreads)
+            p.out[before + i] = s_vals[p.n_table + i];
     }
 }
 
@@ -616,7 +752,6 @@ hipError_t launch_huff(const HuffParams &p, hipStream_t s)
         return hipErrorInvalidValue;
     const dim3 block(kHuffThreads);
     const dim3 grid((unsigned)p.nblk);
-    hipLaunchKernelGGL(k_huff_table, dim3(1), block, 0, s, p);
     hipLaunchKernelGGL(k_huff_parse, grid, block, 0, s, p);
     hipLaunchKernelGGL(k_huff_fix, dim3(1), block, 0, s, p);
     hipLaunchKernelGGL(k_huff_write, grid, block, 0, s, p);

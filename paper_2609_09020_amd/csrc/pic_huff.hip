@@ -15,7 +15,7 @@ struct pic_huff {
     int64_t scratch_bytes;
     char *d_scratch;
     // offsets of the scratch arrays
-    size_t o_lut, o_tab, o_sorted, o_mask, o_end, o_cnt, o_fail, o_flags, o_blk;
+    size_t o_mask, o_end, o_cnt, o_fail, o_flags, o_blk, o_bnd;
 };
 
 namespace {
@@ -69,15 +69,13 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
     h->max_nsub = (int32_t)((d->max_bits + pic::kHuffSub - 1) / pic::kHuffSub);
     const size_t nblk = (size_t)(h->max_nsub + pic::kHuffOwn - 1) / pic::kHuffOwn;
     size_t o = 0;
-    h->o_lut = o;    o += align256(sizeof(uint32_t) << pic::kHuffLutBits);
-    h->o_tab = o;    o += align256(sizeof(int32_t) * 128);
-    h->o_sorted = o; o += align256(sizeof(int32_t) * pic::kHuffMaxTable);
-    h->o_mask = o;   o += align256(16 * (size_t)h->max_nsub);
+    h->o_mask = o;   o += align256(sizeof(uint64_t) * (size_t)h->max_nsub);
     h->o_end = o;    o += align256(sizeof(int32_t) * (size_t)h->max_nsub);
     h->o_cnt = o;    o += align256(sizeof(int32_t) * (size_t)h->max_nsub);
     h->o_fail = o;   o += align256(sizeof(uint32_t) * 8 * nblk);       // two words per wave
     h->o_flags = o;  o += align256(sizeof(int32_t) * 4);
     h->o_blk = o;    o += align256(sizeof(int32_t) * nblk);
+    h->o_bnd = o;    o += align256(sizeof(int32_t) * nblk);
     h->scratch_bytes = (int64_t)o;
     void *mem = nullptr;
     if (hipMalloc(&mem, o) != hipSuccess) {
@@ -122,15 +120,13 @@ pic_status pic_huff_decode(pic_huff *h, const uint8_t *data, int64_t n_bits, con
     p.lengths = lengths;
     p.out = out;
     p.status = status;
-    p.lut = reinterpret_cast<uint32_t *>(h->d_scratch + h->o_lut);
-    p.tab = reinterpret_cast<int32_t *>(h->d_scratch + h->o_tab);
-    p.sorted = reinterpret_cast<int32_t *>(h->d_scratch + h->o_sorted);
-    p.mask = reinterpret_cast<uint32_t *>(h->d_scratch + h->o_mask);
+    p.mask = reinterpret_cast<uint64_t *>(h->d_scratch + h->o_mask);
     p.end = reinterpret_cast<int32_t *>(h->d_scratch + h->o_end);
     p.cnt = reinterpret_cast<int32_t *>(h->d_scratch + h->o_cnt);
     p.fail = reinterpret_cast<uint32_t *>(h->d_scratch + h->o_fail);
     p.flags = reinterpret_cast<int32_t *>(h->d_scratch + h->o_flags);
     p.blk = reinterpret_cast<int32_t *>(h->d_scratch + h->o_blk);
+    p.bnd = reinterpret_cast<int32_t *>(h->d_scratch + h->o_bnd);
     p.nblk = (p.nsub + pic::kHuffOwn - 1) / pic::kHuffOwn;
     p.blk_is_prefix = p.nblk > pic::kHuffPrefixInKernelMax;
     if (pic::launch_huff(p, (hipStream_t)stream) != hipSuccess) {

@@ -91,7 +91,7 @@ hipError_t launch_zpr(const ZprParams &p, bool coeff_only, hipStream_t s);
 namespace pic {
 
 constexpr int kHuffThreads = 256;
-constexpr int kHuffSub = 128;                  // bitstream bits per parsing thread
+constexpr int kHuffSub = 64;                   // bitstream bits per parsing thread
 constexpr int kHuffOwn = kHuffThreads - 1;     // subsequences a workgroup owns (its first thread
                                                // re-parses the previous workgroup's last one)
 constexpr int kHuffPrefixInKernelMax = 4096;   // more workgroups: the fix kernel turns the
@@ -112,20 +112,18 @@ struct HuffParams {
     int32_t *out;                   // [n_symbols]
     int32_t *status;
     // scratch
-    uint32_t *lut;                  // [1 << kHuffLutBits]: index | length << 16, 0 = longer code
-    int32_t *tab;                   // [0]: table valid, [1]: longest length,
-                                    // [8 + l]: first code, [40 + l]: count, [72 + l]: first index of length l
-    int32_t *sorted;                // [kHuffMaxTable] symbol values in code order
-    uint32_t *mask;                 // [nsub][4]: codeword starts of the subsequence's parse
+    uint64_t *mask;                 // [nsub]: codeword starts of the subsequence's parse (bit k: offset k)
     int32_t *end;                   // [nsub]: where that parse crosses into the next subsequence, -1 if it
                                     // met a pattern that is no codeword, n_bits if the stream ran out
     int32_t *cnt;                   // [nsub]: codewords of the true parse that start in the subsequence
     uint32_t *fail;                 // [8 per workgroup]: owned subsequences left out of step (bit l: the
                                     // workgroup's thread l)
-    int32_t *flags;                 // [0]: some subsequence was out of step; [1]: first subsequence
-                                    // whose true parse meets a pattern that is no codeword
+    int32_t *flags;                 // [1]: first subsequence whose true parse meets a pattern that is no
+                                    // codeword
     int32_t *blk;                   // [ceil(nsub / kHuffOwn)]: symbols per workgroup (exclusive prefixes
                                     // when blk_is_prefix)
+    int32_t *bnd;                   // [ceil(nsub / kHuffOwn)]: bit 0: the workgroup's last crossing point
+                                    // moved; bit 1: the workgroup left subsequences to the fix kernel
     int32_t nblk;                   // workgroups of the parse and write kernels
     int32_t blk_is_prefix;
 };

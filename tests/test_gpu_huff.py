@@ -263,7 +263,7 @@ def test_argument_rejection():
         a[6] = 0
         assert D.pic_huff_decode(*a) == D.PIC_OK                 # nothing to decode
         info = h.info()
-        assert info["bits_per_thread"] == 128 and info["lut_bits"] == 11 and info["max_bits"] == 4096
+        assert info["bits_per_thread"] == 64 and info["lut_bits"] == 11 and info["max_bits"] == 4096
 
 
 def test_full_decoder_chain(orc):
