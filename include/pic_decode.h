@@ -75,8 +75,15 @@ typedef enum pic_variant {
     PIC_VARIANT_AUTO = 0,
     PIC_VARIANT_VALU = 1,       /* fp32 vector ALU, canonical order                 */
     PIC_VARIANT_MFMA_F32 = 2,   /* fp32 matrix cores (v_mfma_f32_16x16x4_f32)       */
-    PIC_VARIANT_MFMA_BF16 = 3   /* bf16 matrix cores; requires PIC_BF16 weights;
+    PIC_VARIANT_MFMA_BF16 = 3,  /* bf16 matrix cores; requires PIC_BF16 weights;
                                    activations split into bf16 high + low parts    */
+    PIC_VARIANT_MFMA_F16X3 = 4  /* fp16 matrix cores (v_mfma_f32_16x16x32_f16) at
+                                   binary32 accuracy: each fp32 weight and
+                                   activation is split into two fp16 parts and
+                                   every product is formed from three partial
+                                   products; requires PIC_F32 weights and
+                                   weights, latents and activations below 2^15
+                                   in magnitude (the fp16 range)                   */
 } pic_variant;
 
 enum {

@@ -70,6 +70,39 @@ __device__ __forceinline__ LayerParams layer_params(const DecodeParams &p, int l
 
 // max(x, 0) for a non-NaN float as one integer max: non-negative floats order
 // like their bit patterns, negative ones (sign bit set) are negative integers.
+// Parameter staging in two phases, so that every global load of a workgroup's
+// prologue is in flight before the first one is waited for: load_part reads
+// entries threadIdx.x, + kThreads, ... of a COUNT-entry table into registers,
+// store_part writes them to LDS.
+template <int COUNT, class T>
+struct Part {
+    static constexpr int kPer = (COUNT + kThreads - 1) / kThreads;
+    T v[kPer];
+};
+
+template <int COUNT, class T, class F>
+__device__ __forceinline__ Part<COUNT, T> load_part(F value)
+{
+    Part<COUNT, T> r;
+#pragma unroll
+    for (int i = 0; i < Part<COUNT, T>::kPer; ++i) {
+        const int s = (int)threadIdx.x + i * kThreads;
+        r.v[i] = s < COUNT ? value(s) : T(0);
+    }
+    return r;
+}
+
+template <int COUNT, class T>
+__device__ __forceinline__ void store_part(T *dst, const Part<COUNT, T> &r)
+{
+#pragma unroll
+    for (int i = 0; i < Part<COUNT, T>::kPer; ++i) {
+        const int s = (int)threadIdx.x + i * kThreads;
+        if (s < COUNT)
+            dst[s] = r.v[i];
+    }
+}
+
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
 // Sum of x over the four 16-lane rows of the wavefront, in every lane:

@@ -84,12 +84,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     if (blk < tiles)
         load_boxes<4 * LPG>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
 
-    // ---- stage this image's parameters into LDS in operand layouts
+    // ---- stage this image's parameters into LDS in operand layouts (every
+    // load in flight before the first store)
     {
         const int N1 = p.widths[1];
         const LayerParams l0 = layer_params(p, 0, b);
-#pragma unroll 1
-        for (int s = tid; s < NB * 64 * 4; s += kThreads) {           // layer 1, A layout
+        const auto w1a = load_part<NB * 64 * 4, unsigned>([&](int s) {        // layer 1, A layout
             const int u = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
             const int out = 16 * ob + (ln & 15), gg = ln >> 4;
             unsigned w = 0;
@@ -99,14 +99,14 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                 if (j < LPG && lvl < L && out < N1)
                     w |= l0.bits(out * L + lvl) << (16 * h);
             }
-            ldsu[LY::W1A + s] = w;
-        }
+            return w;
+        });
+        Part<NB * KS2 * 64 * 4, unsigned> wha[NH > 0 ? NH : 1];
 #pragma unroll
-        for (int hl = 0; hl < NH; ++hl) {                              // hidden layers, A layout
+        for (int hl = 0; hl < NH; ++hl) {                                      // hidden layers, A layout
             const int fin = p.widths[1 + hl], fout = p.widths[2 + hl];
             const LayerParams lh = layer_params(p, 1 + hl, b);
-#pragma unroll 1
-            for (int s = tid; s < NB * KS2 * 64 * 4; s += kThreads) {
+            wha[hl] = load_part<NB * KS2 * 64 * 4, unsigned>([&](int s) {
                 const int u = s & 3, ln = (s >> 2) & 63, rest = s >> 8;
                 const int st = rest % KS2, ob = rest / KS2;
                 const int out = 16 * ob + (ln & 15), gg = ln >> 4;
@@ -118,28 +118,35 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                     if (out < fout && in < fin)
                         w |= lh.bits(out * fin + in) << (16 * h);
                 }
-                ldsu[LY::WHA + hl * NB * KS2 * 256 + s] = w;
-            }
+                return w;
+            });
         }
+        Part<NB * 256, float> bias[NH + 1];
 #pragma unroll
-        for (int hl = 0; hl <= NH; ++hl) {                             // biases, accumulator layout
+        for (int hl = 0; hl <= NH; ++hl) {                                     // biases, accumulator layout
             const int fout = p.widths[1 + hl];
-            const float *bias = layer_params(p, hl, b).b;
-#pragma unroll 1
-            for (int s = tid; s < NB * 256; s += kThreads) {
+            const float *bp = layer_params(p, hl, b).b;
+            bias[hl] = load_part<NB * 256, float>([&](int s) {
                 const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
                 const int n = 16 * ob + 4 * (ln >> 4) + r;
-                lds[LY::B1 + hl * NB * 256 + s] = n < fout ? bias[n] : 0.0f;
-            }
+                return n < fout ? bp[n] : 0.0f;
+            });
         }
         const int NL = p.widths[NH + 1];
         const LayerParams lo = layer_params(p, NH + 1, b);
-#pragma unroll 1
-        for (int s = tid; s < NB * 64; s += kThreads) {                // output layer [ob][r][g][c]
+        const auto w3 = load_part<NB * 64, float>([&](int s) {                // output layer [ob][r][g][c]
             const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
             const int n = 16 * ob + 4 * gg + r;
-            lds[LY::W3 + s] = (c < 3 && n < NL) ? lo.weight(c * NL + n) : 0.0f;
-        }
+            return (c < 3 && n < NL) ? lo.weight(c * NL + n) : 0.0f;
+        });
+        store_part(ldsu + LY::W1A, w1a);
+#pragma unroll
+        for (int hl = 0; hl < NH; ++hl)
+            store_part(ldsu + LY::WHA + hl * NB * KS2 * 256, wha[hl]);
+#pragma unroll
+        for (int hl = 0; hl <= NH; ++hl)
+            store_part(lds + LY::B1 + hl * NB * 256, bias[hl]);
+        store_part(lds + LY::W3, w3);
     }
     const float *b3 = layer_params(p, NH + 1, b).b;
     const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];

@@ -57,6 +57,12 @@ struct Layout {
     static constexpr int W3 = BH + NH * NB * 64 * 4;                // [NB][4 r][4 g][4 c]
     static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent boxes
     static constexpr int SIZE = LAT + box_offset(4 * LS);
+    // the parameters as the caller lays them out are first staged in the
+    // regions their operand layouts then replace (each is at least as large)
+    static constexpr int N = 16 * NB;
+    static_assert(N * 4 * LS <= NB * LS * 64, "layer 1 fits its region");
+    static_assert(N * N <= NB * KSH4 * 256 || KSH < 4 * NB, "hidden layers fit their regions");
+    static_assert(3 * N <= NB * 64, "output layer fits its region");
 };
 
 // Neuron on row `row` of an output block; the map is its own inverse.
@@ -85,50 +91,88 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     if (blk < tiles)
         load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
 
-    // ---- stage this image's parameters into LDS in operand layouts
+    // ---- stage this image's parameters into LDS in operand layouts: first
+    // as the caller lays them out, with contiguous loads all in flight at
+    // once, then permuted through registers
     {
         const int N1 = p.widths[1];
         const LayerParams l0 = layer_params(p, 0, b);
-#pragma unroll 1
-        for (int s = tid; s < NB * LS * 64; s += kThreads) {          // layer 1, A layout
+        const int NL = p.widths[NH + 1];
+        const LayerParams lo = layer_params(p, NH + 1, b);
+        constexpr int KSH4 = LY::KSH4;
+        // raw copies: layer 1 in W1A, hidden layer h in its WHA block (or, when
+        // the last K steps are skipped and the block is smaller, in the box
+        // area), the output layer in W3, biases in B1 / BH
+        constexpr int RAW_H = LY::N * LY::N <= NB * KSH4 * 256 ? 0 : 1;
+        static_assert(!RAW_H || NH * LY::N * LY::N <= box_offset(4 * LS), "hidden layers fit the box area");
+        auto raw_h = [&](int h) { return RAW_H ? LY::LAT + h * LY::N * LY::N : LY::WHA + h * NB * KSH4 * 256; };
+        const auto r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return s < N1 * L ? l0.weight(s) : 0.0f; });
+        Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+            const int n = p.widths[1 + h] * p.widths[2 + h];
+            const LayerParams lh = layer_params(p, 1 + h, b);
+            rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return s < n ? lh.weight(s) : 0.0f; });
+        }
+        const auto r3 = load_part<3 * LY::N, float>([&](int s) { return s < 3 * NL ? lo.weight(s) : 0.0f; });
+        Part<LY::N, float> rb[NH + 1];
+#pragma unroll
+        for (int h = 0; h <= NH; ++h) {
+            const int fout = p.widths[1 + h];
+            const float *bp = layer_params(p, h, b).b;
+            rb[h] = load_part<LY::N, float>([&](int s) { return s < fout ? bp[s] : 0.0f; });
+        }
+        store_part(lds + LY::W1A, r1);
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+            store_part(lds + raw_h(h), rh[h]);
+        store_part(lds + LY::W3, r3);
+#pragma unroll
+        for (int h = 0; h <= NH; ++h)
+            store_part(lds + LY::B1 + h * NB * 256, rb[h]);
+        __syncthreads();
+
+        const auto w1a = load_part<NB * LS * 64, float>([&](int s) {          // layer 1, A layout
             const int ln = s & 63, step = (s >> 6) % LS, ob = (s >> 6) / LS;
             const int out = 16 * ob + row_neuron(ln & 15), in = 4 * step + (ln >> 4);
-            lds[LY::W1A + s] = (out < N1 && in < L) ? l0.weight(out * L + in) : 0.0f;
-        }
-        constexpr int KSH4 = LY::KSH4;
+            return (out < N1 && in < L) ? lds[LY::W1A + out * L + in] : 0.0f;
+        });
+        Part<NB * KSH4 * 256, float> wha[NH > 0 ? NH : 1];
 #pragma unroll
-        for (int h = 0; h < NH; ++h) {                                 // hidden layers, A layout
+        for (int h = 0; h < NH; ++h) {                                         // hidden layers, A layout
             const int fin = p.widths[1 + h], fout = p.widths[2 + h];
-            const LayerParams lh = layer_params(p, 1 + h, b);
-#pragma unroll 1
-            for (int s = tid; s < NB * KSH4 * 256; s += kThreads) {
+            wha[h] = load_part<NB * KSH4 * 256, float>([&](int s) {
                 const int j = s & 3, ln = (s >> 2) & 63, q = (s >> 8) % KSH4, ob = (s >> 8) / KSH4;
                 const int ks = 4 * q + j;
                 const int out = 16 * ob + row_neuron(ln & 15);
                 const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
-                lds[LY::WHA + h * NB * KSH4 * 256 + s] =
-                    (ks < KSH && out < fout && in < fin) ? lh.weight(out * fin + in) : 0.0f;
-            }
+                return (ks < KSH && out < fout && in < fin) ? lds[raw_h(h) + out * fin + in] : 0.0f;
+            });
         }
+        Part<NB * 256, float> bias[NH + 1];
 #pragma unroll
-        for (int h = 0; h <= NH; ++h) {                                // biases, accumulator layout
+        for (int h = 0; h <= NH; ++h) {                                        // biases, accumulator layout
             const int fout = p.widths[1 + h];
-            const float *bias = layer_params(p, h, b).b;
-#pragma unroll 1
-            for (int s = tid; s < NB * 256; s += kThreads) {
+            bias[h] = load_part<NB * 256, float>([&](int s) {
                 const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
                 const int n = 16 * ob + 4 * r + (ln >> 4);
-                lds[LY::B1 + h * NB * 256 + s] = n < fout ? bias[n] : 0.0f;
-            }
+                return n < fout ? lds[LY::B1 + h * NB * 256 + n] : 0.0f;
+            });
         }
-        const int NL = p.widths[NH + 1];
-        const LayerParams lo = layer_params(p, NH + 1, b);
-#pragma unroll 1
-        for (int s = tid; s < NB * 64; s += kThreads) {                // output layer [ob][r][g][c]
+        const auto w3 = load_part<NB * 64, float>([&](int s) {                // output layer [ob][r][g][c]
             const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
             const int n = 16 * ob + 4 * r + gg;
-            lds[LY::W3 + s] = (c < 3 && n < NL) ? lo.weight(c * NL + n) : 0.0f;
-        }
+            return (c < 3 && n < NL) ? lds[LY::W3 + c * NL + n] : 0.0f;
+        });
+        __syncthreads();                   // every raw value is read
+        store_part(lds + LY::W1A, w1a);
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+            store_part(lds + LY::WHA + h * NB * KSH4 * 256, wha[h]);
+#pragma unroll
+        for (int h = 0; h <= NH; ++h)
+            store_part(lds + LY::B1 + h * NB * 256, bias[h]);
+        store_part(lds + LY::W3, w3);
     }
     const float *b3 = layer_params(p, NH + 1, b).b;
     const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];

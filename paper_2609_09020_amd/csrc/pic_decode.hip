@@ -49,7 +49,7 @@ pic_status validate_desc(const pic_decode_desc *d)
         return PIC_E_INVALID;
     if (d->max_batch < 1 || d->max_batch > PIC_MAX_BATCH)
         return PIC_E_INVALID;
-    if (d->variant < PIC_VARIANT_AUTO || d->variant > PIC_VARIANT_MFMA_BF16)
+    if (d->variant < PIC_VARIANT_AUTO || d->variant > PIC_VARIANT_MFMA_F16X3)
         return PIC_E_INVALID;
     return PIC_OK;
 }
@@ -97,6 +97,9 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
     case PIC_VARIANT_MFMA_F32: ok = pic::mfma_f32_supports(L, nl, desc->widths); break;
     case PIC_VARIANT_MFMA_BF16:
         ok = desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths);
+        break;
+    case PIC_VARIANT_MFMA_F16X3:
+        ok = desc->weight_dtype == PIC_F32 && pic::mfma_f16x3_supports(L, nl, desc->widths);
         break;
     }
     if (!ok)
@@ -184,6 +187,7 @@ pic_status launch(pic_decoder *dec, const pic::DecodeParams &p, void *stream)
     case PIC_VARIANT_VALU: e = pic::launch_valu(p, s, &name, &pxs); break;
     case PIC_VARIANT_MFMA_F32: e = pic::launch_mfma_f32(p, s, &name, &pxs, dec->num_cus); break;
     case PIC_VARIANT_MFMA_BF16: e = pic::launch_mfma_bf16(p, s, &name, &pxs, dec->num_cus); break;
+    case PIC_VARIANT_MFMA_F16X3: e = pic::launch_mfma_f16x3(p, s, &name, &pxs, dec->num_cus); break;
     }
     if (e != hipSuccess) {
         (void)hipGetLastError();

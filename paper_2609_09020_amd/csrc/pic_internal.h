@@ -38,11 +38,14 @@ hipError_t launch_mfma_f32(const DecodeParams &p, hipStream_t s, const char **na
                            int num_cus);
 hipError_t launch_mfma_bf16(const DecodeParams &p, hipStream_t s, const char **name, int *px_per_step,
                             int num_cus);
+hipError_t launch_mfma_f16x3(const DecodeParams &p, hipStream_t s, const char **name, int *px_per_step,
+                             int num_cus);
 
 // Shape support queries used at create time (no device needed).
 bool valu_supports(int L, int nl, const int32_t *widths);
 bool mfma_f32_supports(int L, int nl, const int32_t *widths);
 bool mfma_bf16_supports(int L, int nl, const int32_t *widths);
+bool mfma_f16x3_supports(int L, int nl, const int32_t *widths);
 
 }  // namespace pic
 

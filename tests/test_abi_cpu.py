@@ -93,7 +93,7 @@ def _gpu_present():
     dict(_raw={"num_layers": 9}),
     dict(widths=(4, 65, 3)), dict(widths=(4, 0, 3)), dict(weight_dtype=2), dict(out_dtype=1),
     dict(flags=2), dict(flags=D.PIC_FLAG_NO_CLAMP, out_dtype=D.PIC_U8), dict(max_batch=0),
-    dict(max_batch=70000), dict(variant=9), dict(height=65536, width=32768),
+    dict(max_batch=70000), dict(variant=9), dict(variant=5), dict(height=65536, width=32768),
     dict(widths=(13,) + (16,) * 2 + (3,)),
 ])
 def test_invalid_descriptors(kw):
@@ -110,8 +110,11 @@ def test_bad_struct_size_and_null_out():
 
 
 def test_unsupported_combinations():
-    # the bf16 matrix-core family needs bf16 weights
+    # the bf16 matrix-core family needs bf16 weights, the fp16-split one fp32
     assert _create_status(variant=D.PIC_VARIANT_MFMA_BF16) == D.PIC_E_UNSUPPORTED
+    assert _create_status(variant=D.PIC_VARIANT_MFMA_F16X3, weight_dtype=D.PIC_BF16) == D.PIC_E_UNSUPPORTED
+    # the matrix-core families take 2 to 4 linear layers
+    assert _create_status(variant=D.PIC_VARIANT_MFMA_F16X3, widths=(4, 3)) == D.PIC_E_UNSUPPORTED
 
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")

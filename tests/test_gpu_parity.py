@@ -89,7 +89,7 @@ def _check_u8_band(got, ref_clamped, ref_u8, what):
 
 
 FULL = ["pic64", "kodak768", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k", "kodak768_paper"]
-F32_VARIANTS = ["valu", "mfma_f32"]
+F32_VARIANTS = ["valu", "mfma_f32", "mfma_f16x3"]
 
 
 def _sample_images(batch):
@@ -136,18 +136,19 @@ def test_workload_u8_reference_bit_exact(name):
             assert n == 0
 
 
+@pytest.mark.parametrize("variant", ["mfma_f32", "mfma_f16x3"])
 @pytest.mark.parametrize("name", ["pic64", "kodak768", "kodak768_b64", "clic2048", "uhd4k"])
-def test_workload_u8_mfma_band(name):
+def test_workload_u8_mfma_band(name, variant):
     wl = synth.WORKLOADS[name]
     inp = synth.workload_inputs(wl)
-    got, _ = gpu_decode(inp, variant="mfma_f32", out_dtype="u8")
+    got, _ = gpu_decode(inp, variant=variant, out_dtype="u8")
     for b in _sample_images(inp.batch):
         for rows in _strips(wl.height):
             kw = dict(batch_slice=slice(b, b + 1), rows=rows)
             refc = oracle.decode_inputs(inp, out="clamped", **kw)
             refq = oracle.decode_inputs(inp, out="u8", **kw)
             _check_u8_band(got[b:b + 1, :, rows[0]:rows[1]], refc, refq,
-                           f"{name} mfma_f32 img{b} rows{rows}")
+                           f"{name} {variant} img{b} rows{rows}")
 
 
 # ------------------------------------------------------------------ fuzz
@@ -189,7 +190,7 @@ def _run_case(case, variant):
     inp = synth.make_inputs(H, W, widths[0], widths, batch=batch, seed=seed, latent="normal",
                             latent_scale=1.5, bias="normal", shared_weights=shared)
     nl = len(widths) - 1
-    if variant == "mfma_f32" and not (2 <= nl <= 4):
+    if variant in ("mfma_f32", "mfma_f16x3") and not (2 <= nl <= 4):
         with pytest.raises(D.PicError) as e:
             gpu_decode(inp, variant=variant)
         assert e.value.status == D.PIC_E_UNSUPPORTED
