@@ -46,9 +46,12 @@ extern "C" {
 #define PIC_API
 #endif
 
-/* Opaque decoder handle.  It owns host state only (the validated descriptor,
- * the chosen kernel variant and the device it was created on); it holds no
- * device memory. */
+/* Opaque decoder handle: the validated descriptor, the chosen kernel variant,
+ * the device it was created on, and 8 bytes of device memory per image of
+ * max_batch (the matrix-core kernels' tile counters: workgroups take tiles
+ * from a per-image counter, and each run clears the next run's).  Runs on one
+ * handle must not overlap: enqueue them on one stream, or synchronise between
+ * them. */
 typedef struct pic_decoder pic_decoder;
 
 typedef enum pic_status {
@@ -79,11 +82,10 @@ typedef enum pic_variant {
                                    activations split into bf16 high + low parts    */
     PIC_VARIANT_MFMA_F16X3 = 4  /* fp16 matrix cores (v_mfma_f32_16x16x32_f16) at
                                    binary32 accuracy: each fp32 weight and
-                                   activation is split into two fp16 parts and
-                                   every product is formed from three partial
-                                   products; requires PIC_F32 weights and
-                                   weights, latents and activations below 2^15
-                                   in magnitude (the fp16 range)                   */
+                                   activation is scaled by a power of two, split
+                                   into two fp16 parts, and every product is
+                                   formed from three partial products; requires
+                                   PIC_F32 weights                                 */
 } pic_variant;
 
 enum {
@@ -134,7 +136,8 @@ typedef struct pic_decode_info {
  * Returns PIC_OK; PIC_E_INVALID for a malformed descriptor (sizes, widths,
  * dtypes, flags out of range); PIC_E_UNSUPPORTED for a valid combination no
  * kernel implements (e.g. MFMA_BF16 with fp32 weights); PIC_E_NODEVICE when no
- * gfx950 device is current; PIC_E_NOMEM when the handle cannot be allocated.
+ * gfx950 device is current; PIC_E_NOMEM when the handle cannot be allocated;
+ * PIC_E_HIP when its device memory cannot (allocated and cleared here, once).
  * Defines: Sec. 3.1 (pyramid and upsample), Sec. 4.1 / App. A (MLP).
  */
 PIC_API pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out);
@@ -219,8 +222,8 @@ PIC_API pic_status pic_fuse_modulation(int32_t in, int32_t out, int32_t batch,
  * Returns PIC_E_INVALID for NULL arguments or an unknown info->struct_size. */
 PIC_API pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info);
 
-/* pic_decode_destroy -- free the handle (NULL is accepted).  Does not wait for
- * work enqueued with it; the caller synchronises first if needed. */
+/* pic_decode_destroy -- free the handle and its device memory (NULL is
+ * accepted).  Synchronises the handle's device first. */
 PIC_API void pic_decode_destroy(pic_decoder *dec);
 
 /* pic_status_string -- static description of a status code (never NULL). */

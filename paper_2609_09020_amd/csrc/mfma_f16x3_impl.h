@@ -229,8 +229,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, col = lane & 15;
-    const int b = blockIdx.x / blocks_per_image;
-    const int blk = blockIdx.x - b * blocks_per_image;
+    // images interleave over the grid, so that every image's workgroups are
+    // spread over the dispatch order (older workgroups on a CU run ahead)
+    const int b = blockIdx.x % p.batch;
+    const int blk = blockIdx.x / p.batch;
     const int L = p.L;
 
     // ---- the first tile's latent loads go out first, so their latency
@@ -353,7 +355,15 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
 
-    for (int t = blk; t < tiles; t += blocks_per_image) {
+    // Tiles: the workgroup's first is tile blk; the others come from a
+    // per-image counter (tile blocks_per_image + ticket), so that workgroups
+    // that run faster take more of them.  The grid's first workgroup clears
+    // the counters of the next run.
+    __shared__ int s_next;
+    if (blockIdx.x == 0)
+        for (int i = tid; i < p.tile_ctr_len; i += kThreads)
+            p.tile_ctr_next[i] = 0;
+    for (int t = blk;;) {
         const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
         const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
@@ -362,6 +372,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
             stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
             __syncthreads();
         }
+        int ticket = 0;    // the tile after this one; its latency hides behind the tile
+        if (tid == 0)
+            ticket = atomicAdd(p.tile_ctr + b, 1);
 #pragma unroll
         for (int s = 0; s < LS; ++s)
             lane_level_tile(lv[s], ty0, tx0, tx1, col);
@@ -452,6 +465,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                     store_out(p, orow + 16 * cg, vo);
             }
         }
+        if (tid == 0)
+            s_next = blocks_per_image + ticket;
+        __syncthreads();
+        t = s_next;
+        if (t >= tiles)
+            break;    // uniform
     }
 }
 

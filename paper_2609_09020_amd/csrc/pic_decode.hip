@@ -18,6 +18,8 @@ struct pic_decoder {
     int64_t biases_per_image;
     int32_t px_per_step;
     char kernel_name[64];
+    int32_t *d_ctr;             // [2][max_batch] tile counters, used by alternate runs
+    uint32_t runs;              // matrix-core runs launched so far
 };
 
 namespace {
@@ -131,6 +133,17 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
         d->weights_per_image += (int64_t)desc->widths[l] * desc->widths[l + 1];
         d->biases_per_image += desc->widths[l + 1];
     }
+    const size_t ctr_bytes = sizeof(int32_t) * 2 * (size_t)desc->max_batch;
+    void *mem = nullptr;
+    if (hipMalloc(&mem, ctr_bytes) != hipSuccess || hipMemset(mem, 0, ctr_bytes) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        (void)hipGetLastError();
+        if (mem)
+            (void)hipFree(mem);
+        delete d;
+        return PIC_E_HIP;
+    }
+    d->d_ctr = static_cast<int32_t *>(mem);
     *out = d;
     return PIC_OK;
 }
@@ -172,13 +185,20 @@ pic_status prepare(const pic_decoder *dec, int32_t batch, const float *const *la
     return PIC_OK;
 }
 
-pic_status launch(pic_decoder *dec, const pic::DecodeParams &p, void *stream)
+pic_status launch(pic_decoder *dec, const pic::DecodeParams &params, void *stream)
 {
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != dec->device) {
         (void)hipGetLastError();
         return PIC_E_INVALID;   // the handle belongs to another device
     }
+    // this run's tile counters (cleared by the previous run, or at create)
+    // and the next run's (cleared by this one)
+    pic::DecodeParams p = params;
+    const int32_t mb = dec->desc.max_batch;
+    p.tile_ctr = dec->d_ctr + (dec->runs & 1u) * mb;
+    p.tile_ctr_next = dec->d_ctr + ((dec->runs + 1u) & 1u) * mb;
+    p.tile_ctr_len = mb;
     hipStream_t s = (hipStream_t)stream;
     const char *name = nullptr;
     int pxs = 0;
@@ -193,6 +213,8 @@ pic_status launch(pic_decoder *dec, const pic::DecodeParams &p, void *stream)
         (void)hipGetLastError();
         return PIC_E_HIP;
     }
+    if (dec->variant != PIC_VARIANT_VALU)
+        ++dec->runs;
     if (name) {
         strncpy(dec->kernel_name, name, sizeof dec->kernel_name - 1);
         dec->px_per_step = pxs;
@@ -296,6 +318,20 @@ pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info)
     return PIC_OK;
 }
 
-void pic_decode_destroy(pic_decoder *dec) { delete dec; }
+void pic_decode_destroy(pic_decoder *dec)
+{
+    if (!dec)
+        return;
+    int cur = -1;
+    const bool switch_dev = hipGetDevice(&cur) == hipSuccess && cur != dec->device;
+    if (switch_dev)
+        (void)hipSetDevice(dec->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(dec->d_ctr);
+    if (switch_dev)
+        (void)hipSetDevice(cur);
+    (void)hipGetLastError();
+    delete dec;
+}
 
 }  // extern "C"

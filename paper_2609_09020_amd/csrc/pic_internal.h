@@ -28,6 +28,9 @@ struct DecodeParams {
     int32_t weights_bf16;               // 1: weights are bf16 bit patterns
     int32_t batch;
     int32_t groups_per_image;           // 16-pixel groups per image (MFMA kernels)
+    int32_t *tile_ctr;                  // [batch] tile counters of this run (zero at its start)
+    int32_t *tile_ctr_next;             // [tile_ctr_len] the next run's counters, cleared by this run
+    int32_t tile_ctr_len;               // counters per run (the handle's max_batch)
 };
 
 // Kernel launchers: return hipSuccess or the launch error.  Each checks that

@@ -225,6 +225,26 @@ def test_shared_weights_stride_zero_matches_repeated():
         assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("variant", ["mfma_f32", "mfma_f16x3"])
+def test_handle_reuse_with_changing_batch(variant):
+    # the matrix-core kernels take tiles from per-image counters that each
+    # run clears for the next one: runs of different batch sizes on one
+    # handle must each decode exactly what a fresh handle decodes
+    from paper_2609_09020_amd import Decoder
+    inp = synth.make_inputs(70, 150, 7, (7, 40, 40, 3), batch=5, seed=31, latent="normal", latent_scale=2.0,
+                            bias="normal")
+    lat, w, b = _to_dev(inp)
+    want, _ = gpu_decode(inp, variant=variant, clamp=False)
+    dec = Decoder(inp.height, inp.width, inp.widths, clamp=False, max_batch=5, variant=variant)
+    for n in (5, 2, 5, 1, 3, 5, 4):
+        out = dec.run([t[:n] for t in lat], w[:n], b[:n])
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        print(f"PARITY handle reuse {variant} batch {n}", flush=True)
+        assert np.array_equal(got, want[:n]), n
+    dec.close()
+
+
 def test_batch_zero_enqueues_nothing():
     from paper_2609_09020_amd import Decoder
     inp = synth.make_inputs(8, 8, 2, (2, 4, 3), batch=1, seed=0)
