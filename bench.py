@@ -32,6 +32,7 @@ METRIC = "decoded Mpixel/s (and FPS at 768x512) on 1 MI355X; % of roofline"
 # MI355X published peaks.
 PEAK_FP32_TFLOPS = 157.3        # fp32 vector (packed) and fp32 matrix
 PEAK_BF16_TFLOPS = 2500.0       # dense bf16 matrix
+PEAK_FP16_TFLOPS = 2500.0       # dense fp16 matrix
 PEAK_HBM_GBS = 8000.0
 
 
@@ -66,10 +67,13 @@ def load_traffic(kernel, workload, out_dtype):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    src = os.path.join(ROOT, "paper_2609_09020_amd", "csrc", kv.get("source", ""))
-    if not os.path.exists(src):
-        return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in kv.get("source", "").split():
+        src = os.path.join(ROOT, "paper_2609_09020_amd", "csrc", name)
+        if not os.path.exists(src):
+            return None
+        h.update(open(src, "rb").read())
+    sha = h.hexdigest()[:16]
     if sha != kv.get("source_sha256_16"):
         return None
     try:
@@ -480,6 +484,10 @@ def main():
         bound, peak, unit = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s"
     elif info["variant"] == "mfma_f32":
         bound, peak, unit = "mfma", PEAK_FP32_TFLOPS, "TFLOP/s"
+    elif info["variant"] == "mfma_f16x3":
+        # fp32 arithmetic carried out on the fp16 matrix cores: against the
+        # peak of the instructions it runs on (its fp32-equivalent rate beside)
+        bound, peak, unit = "mfma", PEAK_FP16_TFLOPS, "TFLOP/s"
     else:
         bound, peak, unit = "alu", PEAK_FP32_TFLOPS, "TFLOP/s"
     achieved = flop / (kern_avg_ms * 1e-3) / 1e12
@@ -498,6 +506,7 @@ def main():
                    "variant": info["variant"], "kernel": kernel, "parallelism": "single GPU"},
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "fp32_equivalent_frac": round(achieved / PEAK_FP32_TFLOPS, 4),
                      "flop_per_launch": flop, "flop_per_pixel": fpp,
                      "compulsory_bytes_per_launch": bytes_per_call(wl, args.out_dtype),
                      "hbm_frac_at_compulsory_bytes": round(

@@ -188,6 +188,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     // that run faster take more of them.  The grid's first workgroup clears
     // the counters of the next run.
     __shared__ int s_next;
+    const bool dynamic = blocks_per_image < tiles;
     if (blockIdx.x == 0)
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
-        if (tid == 0)
+        if (dynamic && tid == 0)
             ticket = atomicAdd(p.tile_ctr + b, 1);
 #pragma unroll
         for (int j = 0; j < LPG; ++j)
@@ -311,6 +312,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                     store_out(p, orow + 16 * cg, v);
             }
         }
+        if (!dynamic)
+            break;    // uniform: one tile per workgroup
         if (tid == 0)
             s_next = blocks_per_image + ticket;
         __syncthreads();

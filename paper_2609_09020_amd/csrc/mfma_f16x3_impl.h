@@ -360,6 +360,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     // that run faster take more of them.  The grid's first workgroup clears
     // the counters of the next run.
     __shared__ int s_next;
+    const bool dynamic = blocks_per_image < tiles;
     if (blockIdx.x == 0)
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
@@ -373,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
-        if (tid == 0)
+        if (dynamic && tid == 0)
             ticket = atomicAdd(p.tile_ctr + b, 1);
 #pragma unroll
         for (int s = 0; s < LS; ++s)
@@ -465,6 +466,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                     store_out(p, orow + 16 * cg, vo);
             }
         }
+        if (!dynamic)
+            break;    // uniform: one tile per workgroup
         if (tid == 0)
             s_next = blocks_per_image + ticket;
         __syncthreads();

@@ -212,6 +212,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     // that run faster take more of them.  The grid's first workgroup clears
     // the counters of the next run.
     __shared__ int s_next;
+    const bool dynamic = blocks_per_image < tiles;
     if (blockIdx.x == 0)
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
@@ -225,7 +226,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
-        if (tid == 0)
+        if (dynamic && tid == 0)
             ticket = atomicAdd(p.tile_ctr + b, 1);
 #pragma unroll
         for (int s = 0; s < LS; ++s)
@@ -314,6 +315,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                     store_out(p, orow + 16 * cg, v);
             }
         }
+        if (!dynamic)
+            break;    // uniform: one tile per workgroup
         if (tid == 0)
             s_next = blocks_per_image + ticket;
         __syncthreads();
