@@ -92,6 +92,15 @@ __device__ __forceinline__ Part<COUNT, T> load_part(F value)
     return r;
 }
 
+// base[idx] if ok, else 0, without a branch: an entry that holds nothing
+// reads base[0] and discards it, so that the LDS reads of every entry a
+// thread gathers can be in flight together.
+__device__ __forceinline__ float lds_or_zero(const float *base, bool ok, int idx)
+{
+    const float v = base[ok ? idx : 0];
+    return ok ? v : 0.0f;
+}
+
 template <int COUNT, class T>
 __device__ __forceinline__ void store_part(T *dst, const Part<COUNT, T> &r)
 {

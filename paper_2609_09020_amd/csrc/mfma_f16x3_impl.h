@@ -128,28 +128,26 @@ template <int Q>
 __device__ __forceinline__ unsigned a_entry(const float *raw, int fin, int fout, int ob, int s, int lane, int w,
                                             float wsc)
 {
+    // Branch-free, so that the reads of all entries a thread forms can be in
+    // flight together: an entry that holds no weight reads raw[0] and
+    // discards it.
     constexpr int T = (Q + 1) / 2;
     const int g = lane >> 4, out = 16 * ob + row_neuron(lane & 15);
     const int p = 4 * s + w;
-    float h0 = 0.0f, h1 = 0.0f;
-    if (out < fout) {
-        if (p < Q) {
-            const int in = 4 * p + g;
-            if (in < fin) {
-                float lo;
-                split_weight(raw[out * fin + in] * wsc, h0, lo);
-                h1 = h0;
-            }
-        } else if (p < Q + T) {
-            const int t = p - Q;
-            const int in0 = 4 * (2 * t) + g, in1 = 4 * (2 * t + 1) + g;
-            float hh;
-            if (in0 < fin)
-                split_weight(raw[out * fin + in0] * wsc, hh, h0);
-            if (2 * t + 1 < Q && in1 < fin)
-                split_weight(raw[out * fin + in1] * wsc, hh, h1);
-        }
-    }
+    const bool pair = p >= Q;   // slots Q .. Q+T-1 hold the low parts of two inputs
+    const int t = p - Q;
+    const int in0 = pair ? 4 * (2 * t) + g : 4 * p + g;
+    const int in1 = 4 * (2 * t + 1) + g;
+    const bool live = out < fout && p < Q + T;
+    const bool ok0 = live && in0 < fin;
+    const bool ok1 = live && pair && 2 * t + 1 < Q && in1 < fin;
+    const float x0 = raw[ok0 ? out * fin + in0 : 0] * wsc;
+    const float x1 = raw[ok1 ? out * fin + in1 : 0] * wsc;
+    float hi0, lo0, hi1, lo1;
+    split_weight(x0, hi0, lo0);
+    split_weight(x1, hi1, lo1);
+    const float h0 = ok0 ? (pair ? lo0 : hi0) : 0.0f;
+    const float h1 = pair ? (ok1 ? lo1 : 0.0f) : h0;
     return pack_f16(h0, h1);
 }
 
@@ -315,13 +313,13 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
             bias[h] = load_part<NB * 256, float>([&](int s) {
                 const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
                 const int n = 16 * ob + 4 * r + (ln >> 4);
-                return n < fout ? lds[LY::B1 + h * NB * 256 + n] : 0.0f;
+                return lds_or_zero(lds + LY::B1 + h * NB * 256, n < fout, n);
             });
         }
         const auto w3 = load_part<NB * 64, float>([&](int s) {                // output layer [ob][r][g][c]
             const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
             const int n = 16 * ob + 4 * r + gg;
-            return (c < 3 && n < NL) ? lds[LY::W3 + c * NL + n] : 0.0f;
+            return lds_or_zero(lds + LY::W3, c < 3 && n < NL, c * NL + n);
         });
         __syncthreads();                   // every raw value is read
         store_part(ldsu + LY::W1A, w1a);

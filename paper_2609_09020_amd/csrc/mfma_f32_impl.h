@@ -87,11 +87,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const int blk = blockIdx.x / p.batch;
     const int L = p.L;
 
-    // ---- the first tile's latent loads go out first, so their latency
-    // overlaps the parameter gather below
     float boxv[box_regs<4 * LS>()];
-    if (blk < tiles)
-        load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
 
     // ---- stage this image's parameters into LDS in operand layouts: first
     // as the caller lays them out, with contiguous loads all in flight at
@@ -124,6 +120,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
             const float *bp = layer_params(p, h, b).b;
             rb[h] = load_part<LY::N, float>([&](int s) { return s < fout ? bp[s] : 0.0f; });
         }
+        // the first tile's latent loads go out behind the parameters: loads
+        // complete in order, so the permutation below need not wait for them
+        if (blk < tiles)
+            load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
         store_part(lds + LY::W1A, r1);
 #pragma unroll
         for (int h = 0; h < NH; ++h)
@@ -206,6 +206,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
     constexpr int KS1 = KSH;   // live registers of a hidden activation
+    constexpr int W3CH = 6;   // (larger chunks raise the VGPR count of the wider shapes)
 
     // Tiles: the workgroup's first is tile blk; the others come from a
     // per-image counter (tile blocks_per_image + ticket), so that workgroups
@@ -301,14 +302,25 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 
                 // output layer on the vector ALU: partial sums over this lane's
                 // live hidden values, then a sum over the four lane groups
+                // (weights are read W3CH at a time, all before their first use,
+                // so one LDS round trip covers each chunk)
                 float o0 = ob0, o1 = ob1, o2 = ob2;
 #pragma unroll
-                for (int ks = 0; ks < KS1; ++ks) {
-                    const f32x4 w3 = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + (ks * 4 + g) * 4]);
-                    const float hv = d[ks >> 2][ks & 3];
-                    o0 = __builtin_fmaf(w3[0], hv, o0);
-                    o1 = __builtin_fmaf(w3[1], hv, o1);
-                    o2 = __builtin_fmaf(w3[2], hv, o2);
+                for (int k0 = 0; k0 < KS1; k0 += W3CH) {
+                    f32x4 w3[W3CH];
+#pragma unroll
+                    for (int j = 0; j < W3CH; ++j)
+                        if (k0 + j < KS1)
+                            w3[j] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((k0 + j) * 4 + g) * 4]);
+#pragma unroll
+                    for (int j = 0; j < W3CH; ++j) {
+                        if (k0 + j < KS1) {
+                            const float hv = d[(k0 + j) >> 2][(k0 + j) & 3];
+                            o0 = __builtin_fmaf(w3[j][0], hv, o0);
+                            o1 = __builtin_fmaf(w3[j][1], hv, o1);
+                            o2 = __builtin_fmaf(w3[j][2], hv, o2);
+                        }
+                    }
                 }
                 const float v = row_sum3(o0, o1, o2);
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
