@@ -54,11 +54,15 @@ constexpr int kWriteLds = 6144;                              // ints: the table'
 // Big-endian 32-bit word w of the bitstream (bytes outside it read as 0).
 __device__ __forceinline__ uint32_t stream_word(const uint8_t *data, int32_t n_bytes, int64_t w)
 {
+    // branch-free (a byte outside the stream reads byte 0 and is dropped), so
+    // that the loads of all the words a thread stages are in flight together
     uint32_t v = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int64_t i = w * 4 + k;
-        v = (v << 8) | (i >= 0 && i < n_bytes ? (uint32_t)data[i] : 0u);
+        const bool in = i >= 0 && i < n_bytes;
+        const uint32_t byte = data[in ? i : 0];
+        v = (v << 8) | (in ? byte : 0u);
     }
     return v;
 }
@@ -81,7 +85,11 @@ struct SharedTables {
 // other loads are waited for.
 __device__ __forceinline__ int first_length(const HuffParams &p)
 {
-    return (int)threadIdx.x < p.n_table ? (int)p.lengths[threadIdx.x] : -1;
+    // branch-free (the table has at least one entry), so that nothing waits
+    // for the load before its use
+    const bool in = (int)threadIdx.x < p.n_table;
+    const int l = p.lengths[in ? threadIdx.x : 0];
+    return in ? l : -1;
 }
 
 // The length counts, first codes, first indexes and limits of the canonical
@@ -98,8 +106,16 @@ __device__ void build_code(const HuffParams &p, SharedTables &s, int len0)
     if (t == 0)
         s.valid = 1;
     __syncthreads();
-    for (int i = t; i < p.n_table; i += kHuffThreads) {
-        const int l = i == t ? len0 : p.lengths[i];
+    // entry t from len0 outside the loop, so that only that load is waited
+    // for here, not the ones issued after it
+    if (t < p.n_table) {
+        if (len0 < 1 || len0 > kHuffMaxLen)
+            s.valid = 0;
+        else
+            atomicAdd(&s.cnt[len0], 1);
+    }
+    for (int i = t + kHuffThreads; i < p.n_table; i += kHuffThreads) {
+        const int l = p.lengths[i];
         if (l < 1 || l > kHuffMaxLen)
             s.valid = 0;
         else
@@ -190,13 +206,14 @@ __device__ void build_lut(SharedTables &s)
 }
 
 // The table's values in code order (by length, then table order).  Needs
-// build_code; all threads.
-__device__ void build_sorted(const HuffParams &p, SharedTables &s, int32_t *sorted)
+// build_code; all threads.  `len0` and `val0` are entry threadIdx.x's length
+// (first_length) and value, loaded before anything was waited for.
+__device__ void build_sorted(const HuffParams &p, SharedTables &s, int32_t *sorted, int len0, int32_t val0)
 {
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    for (int base = 0; base < p.n_table; base += kHuffThreads) {
-        const int i = base + t;
-        const int l = i < p.n_table ? p.lengths[i] : 0;
+    // one pass per kHuffThreads entries: entry i has length l (0: none) and
+    // value v; its rank among the entries of its length continues s.run
+    auto pass = [&](int l, int32_t v) {
         int in_wave = 0;
         for (int k = 1; k <= kHuffMaxLen; ++k) {
             const uint64_t m = __ballot(l == k);
@@ -210,13 +227,21 @@ __device__ void build_sorted(const HuffParams &p, SharedTables &s, int32_t *sort
             int rank = s.run[l] + in_wave;
             for (int w = 0; w < wave; ++w)
                 rank += s.wcnt[w][l];
-            sorted[s.fi[l] + rank] = p.values[i];
+            sorted[s.fi[l] + rank] = v;
         }
         __syncthreads();
         if (t >= 1 && t <= kHuffMaxLen)
             for (int w = 0; w < kWaves; ++w)
                 s.run[t] += s.wcnt[w][t];
         __syncthreads();
+    };
+    // the first entries from len0 / val0, outside the loop, so that only
+    // those loads are waited for here
+    pass(t < p.n_table ? len0 : 0, val0);
+    for (int base = kHuffThreads; base < p.n_table; base += kHuffThreads) {
+        const int i = base + t;
+        const bool in = i < p.n_table;
+        pass(in ? (int)p.lengths[i] : 0, in ? p.values[i] : 0);
     }
 }
 
@@ -268,23 +293,33 @@ __device__ __forceinline__ int decode_one(uint32_t win, const Decoder &dc, int *
     return len;
 }
 
-// Stage the bitstream words [w0, w0 + kStageWords) in LDS (every load issued
-// before the first is waited for).
-__device__ __forceinline__ void stage_words(const HuffParams &p, uint32_t *words, int64_t w0)
+// The bitstream words [w0, w0 + kStageWords) a workgroup stages in LDS, in
+// two steps: load_words issues the loads into registers (nothing waits for
+// them, so the tables can be built meanwhile), store_words writes them.
+constexpr int kStagePer = (kStageWords + kHuffThreads - 1) / kHuffThreads;
+struct StagedWords {
+    uint32_t v[kStagePer];
+};
+
+__device__ __forceinline__ StagedWords load_words(const HuffParams &p, int64_t w0)
 {
-    constexpr int kPer = (kStageWords + kHuffThreads - 1) / kHuffThreads;
     const int32_t n_bytes = (int32_t)(((int64_t)p.n_bits + 7) >> 3);
-    uint32_t v[kPer];
+    StagedWords sw;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
+    for (int j = 0; j < kStagePer; ++j) {
         const int i = threadIdx.x + j * kHuffThreads;
-        v[j] = i < kStageWords ? stream_word(p.data, n_bytes, w0 + i) : 0u;
+        sw.v[j] = stream_word(p.data, n_bytes, w0 + i);   // (i >= kStageWords: not stored)
     }
+    return sw;
+}
+
+__device__ __forceinline__ void store_words(uint32_t *words, const StagedWords &sw)
+{
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
+    for (int j = 0; j < kStagePer; ++j) {
         const int i = threadIdx.x + j * kHuffThreads;
         if (i < kStageWords)
-            words[i] = v[j];
+            words[i] = sw.v[j];
     }
 }
 
@@ -413,12 +448,16 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
     const int l = threadIdx.x;
     const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;           // first owned subsequence
     const int64_t w0 = ((int64_t)t0 - 1) * kSubWords;            // staged from the one before
+    // every global load goes out first; the tables are built while the
+    // bitstream words are on their way
     const int len0 = first_length(p);
-    stage_words(p, s_words, w0);
+    const StagedWords sw = load_words(p, w0);
     build_code(p, s_tab, len0);
     if (!s_tab.valid)
         return;   // uniform
     build_lut(s_tab);
+    store_words(s_words, sw);
+    __syncthreads();
     const Decoder dc = decoder_of(s_tab);
     const int32_t t = t0 + l - 1;
     const bool live = t >= 0 && t < p.nsub;
@@ -657,18 +696,29 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     const int l = threadIdx.x;
     const int32_t t0 = (int32_t)blockIdx.x * kHuffOwn;
     const int64_t w0 = ((int64_t)t0 - 1) * kSubWords;
+    // every global load whose address is known goes out first; the tables
+    // are built while they are on their way
     const int len0 = first_length(p);
-    stage_words(p, s_words, w0);
+    const int32_t val0 = p.values[l < p.n_table ? l : 0];   // (unused past the table)
+    const StagedWords sw = load_words(p, w0);
+    const int32_t t = t0 + l - 1;
+    const bool rec = l > 0 && t < p.nsub;        // a subsequence this thread owns
+    const int32_t last_good = p.flags[1];
+    const int32_t cnt_t = p.cnt[rec ? t : 0];           // (unused unless rec)
+    const uint64_t mask_t = p.mask[rec ? t : 0];
+    const int32_t blk_before = p.blk_is_prefix ? p.blk[blockIdx.x] : 0;
     build_code(p, s_tab, len0);
     if (!s_tab.valid)
         return;   // uniform
     build_lut(s_tab);
-    build_sorted(p, s_tab, s_vals);
+    build_sorted(p, s_tab, s_vals, len0, val0);
+    store_words(s_words, sw);
+    __syncthreads();
     const Decoder dc = decoder_of(s_tab);
     // symbols before this workgroup's subsequences
     int32_t before;
     if (p.blk_is_prefix) {
-        before = p.blk[blockIdx.x];
+        before = blk_before;
     } else {
         int32_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         for (int j = l; j < (int)blockIdx.x; j += 8 * kHuffThreads) {
@@ -679,10 +729,9 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
         (void)block_sum_incl(((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7])), s_wsum,
                              &before);
     }
-    const int32_t t = t0 + l - 1;
     // subsequences after the first one whose true parse meets a pattern
     // that is no codeword hold nothing decodable
-    const int32_t n = l > 0 && t < p.nsub && t <= p.flags[1] ? p.cnt[t] : 0;
+    const int32_t n = rec && t <= last_good ? cnt_t : 0;
     int32_t blk_total;
     const int32_t o = before + block_sum_incl(n, s_wsum, &blk_total) - n;
     // too few codewords: the bits ran out (unless a pattern that is no
@@ -700,7 +749,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     // the record marks every codeword start of the true parse: the codewords
     // are decoded independently, four at a time
     const SubBits bits = lds_sub(s_words, l * kSubWords);
-    uint64_t m = p.mask[t];
+    uint64_t m = mask_t;
     const int32_t k_end = o + n < p.n_symbols ? n : p.n_symbols - o;
     int32_t *out = staged ? s_vals + p.n_table + (o - before) : p.out + o;
     for (int32_t k = 0; k < k_end; k += 4) {
