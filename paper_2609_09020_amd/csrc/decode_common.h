@@ -56,6 +56,18 @@ struct LayerParams {
         return static_cast<const float *>(w)[idx];
     }
     __device__ __forceinline__ unsigned bits(int idx) const { return static_cast<const uint16_t *>(w)[idx]; }
+    // Entry min(idx, n - 1) (n >= 1) of the weights, known to be bf16 (BF16)
+    // or fp32, and of the bias: a raw copy whose entries past n are never
+    // read, loaded without a branch or a select, so that nothing waits for
+    // the loads before they are stored
+    template <bool BF16>
+    __device__ __forceinline__ float weight_clamped(int idx, int n) const
+    {
+        const int i = idx < n ? idx : n - 1;
+        return BF16 ? __uint_as_float((uint32_t) static_cast<const uint16_t *>(w)[i] << 16)
+                    : static_cast<const float *>(w)[i];
+    }
+    __device__ __forceinline__ float bias_clamped(int idx, int n) const { return b[idx < n ? idx : n - 1]; }
 };
 
 __device__ __forceinline__ LayerParams layer_params(const DecodeParams &p, int l, int b)
@@ -68,8 +80,6 @@ __device__ __forceinline__ LayerParams layer_params(const DecodeParams &p, int l
     return lp;
 }
 
-// max(x, 0) for a non-NaN float as one integer max: non-negative floats order
-// like their bit patterns, negative ones (sign bit set) are negative integers.
 // Parameter staging in two phases, so that every global load of a workgroup's
 // prologue is in flight before the first one is waited for: load_part reads
 // entries threadIdx.x, + kThreads, ... of a COUNT-entry table into registers,
@@ -87,7 +97,10 @@ __device__ __forceinline__ Part<COUNT, T> load_part(F value)
 #pragma unroll
     for (int i = 0; i < Part<COUNT, T>::kPer; ++i) {
         const int s = (int)threadIdx.x + i * kThreads;
-        r.v[i] = s < COUNT ? value(s) : T(0);
+        // (in a last, partial round, threads past the table evaluate its last
+        // entry, which store_part does not store: no branch, so nothing waits
+        // for the round's loads here)
+        r.v[i] = value(s < COUNT ? s : COUNT - 1);
     }
     return r;
 }
@@ -112,6 +125,8 @@ __device__ __forceinline__ void store_part(T *dst, const Part<COUNT, T> &r)
     }
 }
 
+// max(x, 0) for a non-NaN float as one integer max: non-negative floats order
+// like their bit patterns, negative ones (sign bit set) are negative integers.
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
 // Sum of x over the four 16-lane rows of the wavefront, in every lane:
@@ -189,10 +204,10 @@ __device__ __forceinline__ void load_boxes(float (&v)[box_regs<KMAX>()], const D
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
         const float iv = pow2_neg(k);
-        const int kk = k < p.L ? k : 0;   // levels past L load level 0 (never stored)
-        const int hk = p.hk[kk], wk = p.wk[kk];
+        // levels past L load level 0 (their slots repeat it; never stored)
+        const int hk = p.hk[k], wk = p.wk[k];
         const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
-        const float *src = p.lat[kk] + (int64_t)b * hk * wk;
+        const float *src = p.lat[k] + (int64_t)b * hk * wk;
         const int n = box_floats(k), pc = box_pitch(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {

@@ -440,6 +440,7 @@ __device__ __forceinline__ int32_t block_sum_incl(int32_t v, int32_t *s_wsum, in
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
 {
+    warm_kernel_args<sizeof(HuffParams)>();
     __shared__ SharedTables s_tab;
     __shared__ uint32_t s_words[kStageWords];
     __shared__ int32_t s_end[kHuffThreads];
@@ -584,6 +585,7 @@ __device__ bool refix(const HuffParams &p, const Decoder &dc, int u, bool *corru
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
 {
+    warm_kernel_args<sizeof(HuffParams)>();
     constexpr int kList = 2048;            // workgroups to repair listed in LDS
     __shared__ SharedTables s_tab;
     __shared__ int32_t s_list[kList];
@@ -688,6 +690,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
 {
+    warm_kernel_args<sizeof(HuffParams)>();
     __shared__ SharedTables s_tab;
     __shared__ uint32_t s_words[kStageWords];
     __shared__ int32_t s_vals[kWriteLds];

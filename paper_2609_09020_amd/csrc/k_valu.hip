@@ -98,6 +98,7 @@ __device__ __forceinline__ void dense(const float *h, float *g, const float *sW,
 template <int PL, int PW>
 __global__ __launch_bounds__(kThreads) void k_valu(DecodeParams p)
 {
+    warm_kernel_args<sizeof(DecodeParams)>();
     constexpr int PA = PL > PW ? PL : PW;
     __shared__ __attribute__((aligned(16))) float sW[PA * PA > 4 * PA ? PA * PA : 4 * PA];
     __shared__ __attribute__((aligned(16))) float sB[PA];

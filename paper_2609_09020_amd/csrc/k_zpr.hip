@@ -106,6 +106,7 @@ __device__ __forceinline__ int32_t block_inclusive_sum(int32_t v, int32_t *s_wsu
 template <int CH>
 __global__ __launch_bounds__(kZprThreads) void k_zpr_count(ZprParams p)
 {
+    warm_kernel_args<sizeof(ZprParams)>();
     constexpr int SPT = CH / kZprThreads;
     __shared__ int32_t s_wsum[kWaves];
     const int t = threadIdx.x;
@@ -135,6 +136,7 @@ constexpr int kScanSeg = kScanThreads * kScanPer;
 
 __global__ __launch_bounds__(kScanThreads) void k_zpr_scan(ZprParams p)
 {
+    warm_kernel_args<sizeof(ZprParams)>();
     __shared__ int32_t s_seg[kScanSeg];
     __shared__ int32_t s_wsum[kScanThreads / 64];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -227,6 +229,7 @@ __device__ __forceinline__ void idct8(const float in[8], float out[8])
 template <int CH, bool COEFF>
 __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
 {
+    warm_kernel_args<sizeof(ZprParams)>();
     constexpr int NS = kHalo + CH;                 // staged symbols
     constexpr int SPS = NS / kZprThreads;          // per thread, consecutive
     static_assert(NS % kZprThreads == 0, "staging must divide evenly");

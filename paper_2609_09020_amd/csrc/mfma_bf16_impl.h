@@ -71,6 +71,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
     unsigned *ldsu = reinterpret_cast<unsigned *>(lds);
 
+    warm_kernel_args<sizeof(DecodeParams)>();
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, col = lane & 15;

@@ -224,6 +224,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
     unsigned *ldsu = reinterpret_cast<unsigned *>(lds);
 
+    warm_kernel_args<sizeof(DecodeParams)>();
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, col = lane & 15;
@@ -244,25 +245,32 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     // parts and permuted into the operand layouts through registers
     float wsc[NH + 1], winv[NH + 1];
     {
-        const int N1 = p.widths[1];
-        const LayerParams l0 = layer_params(p, 0, b);
-        const int NL = p.widths[NH + 1];
-        const LayerParams lo = layer_params(p, NH + 1, b);
-        const auto r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return s < N1 * L ? l0.weight(s) : 0.0f; });
+        // every layer's pointers and widths first (one batch of scalar
+        // loads), then the raw copies, branch-free (entries past a layer's
+        // size repeat its last entry: the maxima are unchanged and the
+        // permutation reads only valid ones)
+        LayerParams lp[NH + 2];
+        int wd[NH + 3];
+#pragma unroll
+        for (int l = 0; l < NH + 2; ++l)
+            lp[l] = layer_params(p, l, b);
+#pragma unroll
+        for (int l = 0; l < NH + 3; ++l)
+            wd[l] = p.widths[l];
+        const int N1 = wd[1], NL = wd[NH + 1];
+        const auto r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return lp[0].template weight_clamped<false>(s, N1 * L); });
         Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
 #pragma unroll
         for (int h = 0; h < NH; ++h) {
-            const int n = p.widths[1 + h] * p.widths[2 + h];
-            const LayerParams lh = layer_params(p, 1 + h, b);
-            rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return s < n ? lh.weight(s) : 0.0f; });
+            const int n = wd[1 + h] * wd[2 + h];
+            rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return lp[1 + h].template weight_clamped<false>(s, n); });
         }
-        const auto r3 = load_part<3 * LY::N, float>([&](int s) { return s < 3 * NL ? lo.weight(s) : 0.0f; });
+        const auto r3 = load_part<3 * LY::N, float>([&](int s) { return lp[NH + 1].template weight_clamped<false>(s, 3 * NL); });
         Part<LY::N, float> rb[NH + 1];
 #pragma unroll
         for (int h = 0; h <= NH; ++h) {
-            const int fout = p.widths[1 + h];
-            const float *bp = layer_params(p, h, b).b;
-            rb[h] = load_part<LY::N, float>([&](int s) { return s < fout ? bp[s] : 0.0f; });
+            const int fout = wd[1 + h];
+            rb[h] = load_part<LY::N, float>([&](int s) { return lp[h].bias_clamped(s, fout); });
         }
         {
             const float m1 = wave_max(part_max(r1));

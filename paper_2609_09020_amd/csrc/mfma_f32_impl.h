@@ -40,6 +40,8 @@
 //   one integer max, no padding registers touched.
 #pragma once
 
+#include <type_traits>
+
 #include "decode_common.h"
 
 namespace pic {
@@ -78,6 +80,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     using LY = Layout<NB, NH, LS, KSH>;
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
 
+    warm_kernel_args<sizeof(DecodeParams)>();
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, col = lane & 15;
@@ -93,10 +96,19 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     // as the caller lays them out, with contiguous loads all in flight at
     // once, then permuted through registers
     {
-        const int N1 = p.widths[1];
-        const LayerParams l0 = layer_params(p, 0, b);
-        const int NL = p.widths[NH + 1];
-        const LayerParams lo = layer_params(p, NH + 1, b);
+        // every layer's pointers and widths first (one batch of scalar
+        // loads), then the loads themselves: raw copies whose entries past
+        // the layer's size hold anything (the permutation reads only valid
+        // ones), so no load is waited for before the latents' go out
+        LayerParams lp[NH + 2];
+        int wd[NH + 3];
+#pragma unroll
+        for (int l = 0; l < NH + 2; ++l)
+            lp[l] = layer_params(p, l, b);
+#pragma unroll
+        for (int l = 0; l < NH + 3; ++l)
+            wd[l] = p.widths[l];
+        const int N1 = wd[1], NL = wd[NH + 1];
         constexpr int KSH4 = LY::KSH4;
         // raw copies: layer 1 in W1A, hidden layer h in its WHA block (or, when
         // the last K steps are skipped and the block is smaller, in the box
@@ -104,22 +116,30 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         constexpr int RAW_H = LY::N * LY::N <= NB * KSH4 * 256 ? 0 : 1;
         static_assert(!RAW_H || NH * LY::N * LY::N <= box_offset(4 * LS), "hidden layers fit the box area");
         auto raw_h = [&](int h) { return RAW_H ? LY::LAT + h * LY::N * LY::N : LY::WHA + h * NB * KSH4 * 256; };
-        const auto r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return s < N1 * L ? l0.weight(s) : 0.0f; });
-        Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-            const int n = p.widths[1 + h] * p.widths[2 + h];
-            const LayerParams lh = layer_params(p, 1 + h, b);
-            rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return s < n ? lh.weight(s) : 0.0f; });
-        }
-        const auto r3 = load_part<3 * LY::N, float>([&](int s) { return s < 3 * NL ? lo.weight(s) : 0.0f; });
         Part<LY::N, float> rb[NH + 1];
 #pragma unroll
         for (int h = 0; h <= NH; ++h) {
-            const int fout = p.widths[1 + h];
-            const float *bp = layer_params(p, h, b).b;
-            rb[h] = load_part<LY::N, float>([&](int s) { return s < fout ? bp[s] : 0.0f; });
+            const int fout = wd[1 + h];
+            rb[h] = load_part<LY::N, float>([&](int s) { return lp[h].bias_clamped(s, fout); });
         }
+        Part<LY::N * 4 * LS, float> r1;
+        Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
+        Part<3 * LY::N, float> r3;
+        // one straight run of loads per weight type (uniform branch)
+        auto load_weights = [&](auto bf16) {
+            constexpr bool BF = decltype(bf16)::value;
+            r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return lp[0].template weight_clamped<BF>(s, N1 * L); });
+#pragma unroll
+            for (int h = 0; h < NH; ++h) {
+                const int n = wd[1 + h] * wd[2 + h];
+                rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return lp[1 + h].template weight_clamped<BF>(s, n); });
+            }
+            r3 = load_part<3 * LY::N, float>([&](int s) { return lp[NH + 1].template weight_clamped<BF>(s, 3 * NL); });
+        };
+        if (lp[0].bf16)
+            load_weights(std::true_type{});
+        else
+            load_weights(std::false_type{});
         // the first tile's latent loads go out behind the parameters: loads
         // complete in order, so the permutation below need not wait for them
         if (blk < tiles)

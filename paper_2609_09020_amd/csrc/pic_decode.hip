@@ -170,6 +170,11 @@ pic_status prepare(const pic_decoder *dec, int32_t batch, const float *const *la
         p.hk[k] = level_dim(d.height, k);
         p.wk[k] = level_dim(d.width, k);
     }
+    for (int k = d.num_levels; k < PIC_MAX_LEVELS; ++k) {   // unused slots repeat level 0
+        p.lat[k] = p.lat[0];
+        p.hk[k] = p.hk[0];
+        p.wk[k] = p.wk[0];
+    }
     p.H = d.height;
     p.W = d.width;
     p.L = d.num_levels;

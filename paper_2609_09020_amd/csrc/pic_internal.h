@@ -9,10 +9,32 @@
 
 namespace pic {
 
+// Read one dword of every 64-byte line of the kernel arguments, all at once
+// and waited for together, at kernel entry.  The arguments of a launch are
+// written for that launch, so their lines start cold; read where first
+// needed, they would cost a memory round trip per line, one after another
+// (the address of the next load often depends on the previous one).
+template <int BYTES>
+__device__ __forceinline__ void warm_kernel_args()
+{
+    static_assert(BYTES <= 12 * 64, "one operand per line below");
+    const unsigned *ka = (const unsigned *)__builtin_amdgcn_kernarg_segment_ptr();
+    unsigned v[12];
+#pragma unroll
+    for (int i = 0; i < 12; ++i)
+        v[i] = ka[(i * 64 < BYTES ? i * 64 : 0) / 4];
+    // every value used at once: the loads go out together, one wait
+    asm volatile("" ::"s"(v[0]), "s"(v[1]), "s"(v[2]), "s"(v[3]), "s"(v[4]), "s"(v[5]), "s"(v[6]), "s"(v[7]),
+                 "s"(v[8]), "s"(v[9]), "s"(v[10]), "s"(v[11]));
+}
+
 // Output encodings of the epilogue.
 enum OutKind : int32_t { OUT_RAW_F32 = 0, OUT_CLAMPED_F32 = 1, OUT_U8 = 2 };
 
 // Everything a decode kernel needs, passed by value as the kernel argument.
+// Level slots L .. PIC_MAX_LEVELS - 1 repeat level 0, so that an unrolled
+// level loop reads every slot at a constant index (a run-time index into the
+// kernel arguments becomes one waited-for scalar load per level).
 struct DecodeParams {
     const float *lat[PIC_MAX_LEVELS];   // level k base pointer, [batch][hk][wk]
     int32_t hk[PIC_MAX_LEVELS];         // ceil(H / 2^k)
