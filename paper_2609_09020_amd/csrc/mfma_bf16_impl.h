@@ -80,6 +80,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     const int b = blockIdx.x % p.batch;
     const int blk = blockIdx.x / p.batch;
     const int L = p.L;
+    // the output layer's bias, read now so its latency hides behind the
+    // parameter loads
+    const float *b3 = layer_params(p, NH + 1, b).b;
+    const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
 
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
@@ -151,8 +155,6 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             store_part(lds + LY::B1 + hl * NB * 256, bias[hl]);
         store_part(lds + LY::W3, w3);
     }
-    const float *b3 = layer_params(p, NH + 1, b).b;
-    const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
     if (blk < tiles)
         store_boxes<4 * LPG>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
