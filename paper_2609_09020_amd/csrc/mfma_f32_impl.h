@@ -255,11 +255,16 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         for (int s = 0; s < LS; ++s)
             lane_level_tile(lv[s], ty0, tx0, tx1, col);
 
+        // A wavefront's priority is raised for the first row of each tile and
+        // dropped after it, so that the wavefronts of a SIMD progress together
+        // instead of oldest first, and none is left to run alone at the end.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll 1
         for (int rr = 0; rr < 2; ++rr) {
             const int y = ty0 + 2 * wave + rr;
             if (y > ty1)
                 break;   // wave-uniform: the row lies below the image
+
             int roff[LS];
             float rly[LS];
 #pragma unroll
@@ -348,6 +353,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
                     store_out(p, orow + 16 * cg, v);
             }
+            __builtin_amdgcn_s_setprio(0);
         }
         if (!dynamic)
             break;    // uniform: one tile per workgroup
