@@ -83,8 +83,6 @@ __device__ __forceinline__ unsigned pack_f16(float a, float b)
     return __builtin_bit_cast(unsigned, f16x2{(_Float16)a, (_Float16)b});
 }
 
-__device__ __forceinline__ float f16_lo(unsigned v) { return (float)__builtin_bit_cast(f16x2, v)[0]; }
-__device__ __forceinline__ float f16_hi(unsigned v) { return (float)__builtin_bit_cast(f16x2, v)[1]; }
 
 // The fp16 parts of w: (w_h, w_l).
 __device__ __forceinline__ void split_weight(float w, float &h, float &l)
@@ -94,24 +92,28 @@ __device__ __forceinline__ void split_weight(float w, float &h, float &l)
     l = (float)(_Float16)(w - h);
 }
 
-// K entries of a layer's input: the lane group's values v_q, q < Q, as the
-// B operand of ksteps(Q) matrix steps (slot pairs as in the header).
+// K entries of a layer's input: the lane group's values v_q, q < Q, times the
+// power of two sc, as the B operand of ksteps(Q) matrix steps (slot pairs as
+// in the header).  The scaling is exact, so h_q = fp16(sc v_q) and
+// l_q = fp16(sc v_q - h_q), with sc v_q - h_q exact in fp32; each is one
+// mixed-precision FMA (fp32 in, fp16 out).
 template <int Q>
-__device__ __forceinline__ void build_b(const float (&v)[Q], u32x4 (&b)[ksteps(Q)])
+__device__ __forceinline__ void build_b(const float (&v)[Q], float sc, u32x4 (&b)[ksteps(Q)])
 {
     constexpr int T = (Q + 1) / 2;
     unsigned reg[4 * ksteps(Q)];
-    float hi[2 * T];
+    _Float16 hi[2 * T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) {              // (hi, hi) pairs; their halves give every hi part
-        const unsigned pk = pack_f16(v[2 * t], 2 * t + 1 < Q ? v[2 * t + 1] : 0.0f);
-        reg[Q + t] = pk;
-        hi[2 * t] = f16_lo(pk);
-        hi[2 * t + 1] = f16_hi(pk);
+    for (int q = 0; q < 2 * T; ++q)
+        hi[q] = q < Q ? (_Float16)(v[q] * sc) : (_Float16)0.0f;
+#pragma unroll
+    for (int t = 0; t < T; ++t)                // (hi, hi) pairs
+        reg[Q + t] = __builtin_bit_cast(unsigned, f16x2{hi[2 * t], hi[2 * t + 1]});
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {              // (hi, lo)
+        const _Float16 lo = (_Float16)__builtin_fmaf(v[q], sc, -(float)hi[q]);
+        reg[q] = __builtin_bit_cast(unsigned, f16x2{hi[q], lo});
     }
-#pragma unroll
-    for (int q = 0; q < Q; ++q)                // (hi, lo): hi rounds v_q as above, lo the rest
-        reg[q] = pack_f16(v[q], v[q] - hi[q]);
 #pragma unroll
     for (int k = Q + T; k < 4 * ksteps(Q); ++k)
         reg[k] = 0u;
@@ -174,21 +176,16 @@ __device__ __forceinline__ float column_max(float x)
     return fmaxf(__uint_as_float(c[0]), __uint_as_float(c[1]));
 }
 
-// Scale this pixel's inputs of a layer (its values v_q in every lane group)
-// into range; returns the inverse scale.
+// The power of two that brings this pixel's inputs of a layer (its values
+// v_q in every lane group) into range, and its inverse.
 template <int Q>
-__device__ __forceinline__ float scale_inputs(float (&v)[Q])
+__device__ __forceinline__ float input_scale(const float (&v)[Q], float &inv)
 {
     float m = 0.0f;
 #pragma unroll
     for (int q = 0; q < Q; ++q)
         m = fmaxf(m, fabsf(v[q]));
-    float inv;
-    const float sc = scale_for(column_max(m), inv);
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-        v[q] *= sc;
-    return inv;
+    return scale_for(column_max(m), inv);
 }
 
 // Largest magnitude in a part (this thread's entries).
@@ -413,9 +410,11 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
 #pragma unroll
                 for (int s = 0; s < LS; ++s)
                     u[s] = lane_level_sample(lds, lv[s], roff[s], rly[s], cg);
-                const float un1 = scale_inputs<LS>(u) * winv[0];
+                float inv1;
+                const float sc1 = input_scale<LS>(u, inv1);
+                const float un1 = inv1 * winv[0];
                 u32x4 b1[S1];
-                build_b<LS>(u, b1);
+                build_b<LS>(u, sc1, b1);
                 f32x4 d[NB];
 #pragma unroll
                 for (int ob = 0; ob < NB; ++ob)
@@ -437,9 +436,11 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                 // hidden layers
 #pragma unroll
                 for (int h = 0; h < NH; ++h) {
-                    const float unh = scale_inputs<KSH>(v) * winv[1 + h];
+                    float invh;
+                    const float sch = input_scale<KSH>(v, invh);
+                    const float unh = invh * winv[1 + h];
                     u32x4 bh[SH];
-                    build_b<KSH>(v, bh);
+                    build_b<KSH>(v, sch, bh);
                     f32x4 e[NB];
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
@@ -461,13 +462,25 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
 
                 // output layer on the vector ALU: partial sums over this lane's
                 // values, then a sum over the four lane groups
+                // (weights read six values at a time, all before their first
+                // use, so one LDS round trip covers each chunk)
                 float o0 = ob0, o1 = ob1, o2 = ob2;
+                constexpr int W3CH = 6;
 #pragma unroll
-                for (int q = 0; q < KSH; ++q) {
-                    const f32x4 w3 = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + (q * 4 + g) * 4]);
-                    o0 = __builtin_fmaf(w3[0], v[q], o0);
-                    o1 = __builtin_fmaf(w3[1], v[q], o1);
-                    o2 = __builtin_fmaf(w3[2], v[q], o2);
+                for (int q0 = 0; q0 < KSH; q0 += W3CH) {
+                    f32x4 w3[W3CH];
+#pragma unroll
+                    for (int j = 0; j < W3CH; ++j)
+                        if (q0 + j < KSH)
+                            w3[j] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((q0 + j) * 4 + g) * 4]);
+#pragma unroll
+                    for (int j = 0; j < W3CH; ++j) {
+                        if (q0 + j < KSH) {
+                            o0 = __builtin_fmaf(w3[j][0], v[q0 + j], o0);
+                            o1 = __builtin_fmaf(w3[j][1], v[q0 + j], o1);
+                            o2 = __builtin_fmaf(w3[j][2], v[q0 + j], o2);
+                        }
+                    }
                 }
                 const float vo = row_sum3(o0, o1, o2);
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
