@@ -290,20 +290,17 @@ __device__ __forceinline__ float lane_level_sample(const float *lds, const LaneL
     return __builtin_fmaf(ly, bot - top, top);
 }
 
-// Write one output value (lane group g < 3 writes channel g).  The stores
-// are non-temporal: the image is written once and not read back by the
-// kernel, so it need not stay in the caches.
+// Write one output value (lane group g < 3 writes channel g).
 __device__ __forceinline__ void store_out(const DecodeParams &p, int64_t o, float v)
 {
     if (p.out_kind == OUT_RAW_F32) {
-        __builtin_nontemporal_store(v, static_cast<float *>(p.out) + o);
+        static_cast<float *>(p.out)[o] = v;
     } else {
         const float cl = fminf(fmaxf(v, 0.0f), 1.0f);
         if (p.out_kind == OUT_CLAMPED_F32)
-            __builtin_nontemporal_store(cl, static_cast<float *>(p.out) + o);
+            static_cast<float *>(p.out)[o] = cl;
         else
-            __builtin_nontemporal_store((uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f)),
-                                        static_cast<uint8_t *>(p.out) + o);
+            static_cast<uint8_t *>(p.out)[o] = (uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f));
     }
 }
 
