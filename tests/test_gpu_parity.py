@@ -1,6 +1,7 @@
 """GPU parity: the HIP decode path (through the C ABI) against the CPU oracle.
 
-Bars (written here, derived in the design doc):
+Bars (the 8-bit band follows from the 1e-5 bar: an fp32 error within it can
+move 255 c + 1/2 across an integer only from inside the band):
   * fp32 output clamped to [0, 1]: max |gpu - oracle_f64| <= 1e-5;
   * raw output (PIC_FLAG_NO_CLAMP): |gpu - oracle_f64| <= 1e-5 * max(1, |oracle|);
   * 8-bit output, reference (VALU) family: identical to the oracle's binary32
