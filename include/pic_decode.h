@@ -48,10 +48,10 @@ extern "C" {
 
 /* Opaque decoder handle: the validated descriptor, the chosen kernel variant,
  * the device it was created on, and 8 bytes of device memory per image of
- * max_batch (the matrix-core kernels' tile counters: workgroups take tiles
- * from a per-image counter, and each run clears the next run's).  Runs on one
- * handle must not overlap: enqueue them on one stream, or synchronise between
- * them. */
+ * max_batch, at least 64 bytes (the matrix-core kernels' tile counters:
+ * workgroups take tiles from a per-image counter, or from one per XCD for a
+ * single image, and each run clears the next run's).  Runs on one handle must
+ * not overlap: enqueue them on one stream, or synchronise between them. */
 typedef struct pic_decoder pic_decoder;
 
 typedef enum pic_status {

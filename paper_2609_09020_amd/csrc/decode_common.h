@@ -125,6 +125,43 @@ __device__ __forceinline__ void store_part(T *dst, const Part<COUNT, T> &r)
     }
 }
 
+// Tile schedule of a workgroup.  Its first tile is static; when the grid has
+// fewer workgroups than tiles, the others come from a counter: the next tile
+// is base + (the counter's old value), while that is below end.
+// Workgroups are dealt to the 8 XCDs in turn (workgroup i to XCD i mod 8),
+// and each XCD has its own L2.  In a one-image grid (of a multiple of 8
+// workgroups) XCD x therefore takes the contiguous tile range
+// [x tiles / 8, (x + 1) tiles / 8) with a counter of its own, so that the halo
+// rows and columns two neighbouring tiles share are read into one L2.
+// Other grids keep the plain order and one counter per image (batches of a
+// multiple of 8 images keep each image on one XCD anyway, since images
+// interleave over the grid).
+struct TileSchedule {
+    int first;
+    int *ctr;
+    int base, end;
+};
+
+__device__ __forceinline__ TileSchedule tile_schedule(const DecodeParams &p, int block, int bpi, int tiles)
+{
+    TileSchedule ts;
+    if (p.batch == 1 && bpi % kXcds == 0) {
+        const int x = block % kXcds;
+        const int r0 = (int)((int64_t)tiles * x / kXcds);
+        ts.first = r0 + block / kXcds;
+        ts.ctr = p.tile_ctr + x;
+        ts.base = r0 + bpi / kXcds;
+        ts.end = (int)((int64_t)tiles * (x + 1) / kXcds);
+    } else {
+        const int b = block % p.batch;
+        ts.first = block / p.batch;
+        ts.ctr = p.tile_ctr + b;
+        ts.base = bpi;
+        ts.end = tiles;
+    }
+    return ts;
+}
+
 // max(x, 0) for a non-NaN float as one integer max: non-negative floats order
 // like their bit patterns, negative ones (sign bit set) are negative integers.
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }

@@ -78,7 +78,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     // images interleave over the grid, so that every image's workgroups are
     // spread over the dispatch order (older workgroups on a CU run ahead)
     const int b = blockIdx.x % p.batch;
-    const int blk = blockIdx.x / p.batch;
+    const TileSchedule ts = tile_schedule(p, blockIdx.x, blocks_per_image, tiles);
+    const int blk = ts.first;
     const int L = p.L;
     // the output layer's bias, read now so its latency hides behind the
     // parameter loads
@@ -186,10 +187,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
     const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
 
-    // Tiles: the workgroup's first is tile blk; the others come from a
-    // per-image counter (tile blocks_per_image + ticket), so that workgroups
-    // that run faster take more of them.  The grid's first workgroup clears
-    // the counters of the next run.
+    // Tiles: the workgroup's first is tile blk; the others come from its
+    // schedule's counter (tile ts.base + ticket, while below ts.end), so that
+    // workgroups that run faster take more of them.  The grid's first
+    // workgroup clears the counters of the next run.
     __shared__ int s_next;
     const bool dynamic = blocks_per_image < tiles;
     if (blockIdx.x == 0)
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
         if (dynamic && tid == 0)
-            ticket = atomicAdd(p.tile_ctr + b, 1);
+            ticket = atomicAdd(ts.ctr, 1);
 #pragma unroll
         for (int j = 0; j < LPG; ++j)
             lane_level_tile(lv[j], ty0, tx0, tx1, col);
@@ -318,10 +319,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
         if (!dynamic)
             break;    // uniform: one tile per workgroup
         if (tid == 0)
-            s_next = blocks_per_image + ticket;
+            s_next = ts.base + ticket;
         __syncthreads();
         t = s_next;
-        if (t >= tiles)
+        if (t >= ts.end)
             break;    // uniform
     }
 }

@@ -18,7 +18,7 @@ struct pic_decoder {
     int64_t biases_per_image;
     int32_t px_per_step;
     char kernel_name[64];
-    int32_t *d_ctr;             // [2][max_batch] tile counters, used by alternate runs
+    int32_t *d_ctr;             // [2][tile_counters(max_batch)] tile counters, used by alternate runs
     uint32_t runs;              // matrix-core runs launched so far
 };
 
@@ -133,7 +133,7 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
         d->weights_per_image += (int64_t)desc->widths[l] * desc->widths[l + 1];
         d->biases_per_image += desc->widths[l + 1];
     }
-    const size_t ctr_bytes = sizeof(int32_t) * 2 * (size_t)desc->max_batch;
+    const size_t ctr_bytes = sizeof(int32_t) * 2 * (size_t)pic::tile_counters(desc->max_batch);
     void *mem = nullptr;
     if (hipMalloc(&mem, ctr_bytes) != hipSuccess || hipMemset(mem, 0, ctr_bytes) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
@@ -200,7 +200,7 @@ pic_status launch(pic_decoder *dec, const pic::DecodeParams &params, void *strea
     // this run's tile counters (cleared by the previous run, or at create)
     // and the next run's (cleared by this one)
     pic::DecodeParams p = params;
-    const int32_t mb = dec->desc.max_batch;
+    const int32_t mb = pic::tile_counters(dec->desc.max_batch);
     p.tile_ctr = dec->d_ctr + (dec->runs & 1u) * mb;
     p.tile_ctr_next = dec->d_ctr + ((dec->runs + 1u) & 1u) * mb;
     p.tile_ctr_len = mb;

@@ -28,6 +28,11 @@ __device__ __forceinline__ void warm_kernel_args()
                  "s"(v[8]), "s"(v[9]), "s"(v[10]), "s"(v[11]));
 }
 
+// Tile counters a decode handle keeps per run: one per image, and at least
+// one per XCD (a one-image grid schedules each XCD's tiles separately).
+constexpr int kXcds = 8;
+inline int tile_counters(int max_batch) { return max_batch > kXcds ? max_batch : kXcds; }
+
 // Output encodings of the epilogue.
 enum OutKind : int32_t { OUT_RAW_F32 = 0, OUT_CLAMPED_F32 = 1, OUT_U8 = 2 };
 
