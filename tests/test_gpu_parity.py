@@ -246,6 +246,32 @@ def test_handle_reuse_with_changing_batch(variant):
     dec.close()
 
 
+@pytest.mark.parametrize("variant", ["mfma_f32", "mfma_f16x3"])
+def test_one_image_tile_ranges_per_xcd(variant):
+    # a one-image grid takes each XCD's tiles from a contiguous range and a
+    # counter of its own; 1920x1080 has 4050 tiles (not a multiple of 8) and
+    # more tiles than workgroups, so the ranges are uneven and the counters
+    # run.  Every pixel must be written (the output starts as NaN) and match
+    # the oracle on sampled rows, on two runs of one handle.
+    from paper_2609_09020_amd import Decoder
+    H, W = 1080, 1920
+    inp = synth.make_inputs(H, W, 7, (7, 40, 40, 3), seed=5, bias="normal")
+    lat, w, b = _to_dev(inp)
+    dec = Decoder(H, W, inp.widths, clamp=False, max_batch=1, variant=variant)
+    for run in range(2):
+        out = torch.full((1, 3, H, W), float("nan"), device="cuda")
+        dec.run(lat, w, b, out=out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        print(f"PARITY xcd ranges {variant} run {run}: unwritten {int(np.count_nonzero(~np.isfinite(got)))}",
+              flush=True)
+        assert np.isfinite(got).all()
+        for rows in _strips(H):
+            ref = oracle.decode_inputs(inp, out="raw", rows=rows)
+            _check_float(got[:, :, rows[0]:rows[1]], ref, True, f"xcd ranges {variant} run {run} rows{rows}")
+    dec.close()
+
+
 def test_batch_zero_enqueues_nothing():
     from paper_2609_09020_amd import Decoder
     inp = synth.make_inputs(8, 8, 2, (2, 4, 3), batch=1, seed=0)
