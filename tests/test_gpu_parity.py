@@ -55,11 +55,18 @@ def gpu_decode(inp, variant="auto", out_dtype="f32", clamp=True, shared=False, s
     lat, w, b = _to_dev(inp)
     if shared:
         w, b = w[0].contiguous(), b[0].contiguous()
-    out = dec.run(lat, w, b, stream=stream)
+    out = dec.alloc_out(inp.batch, "cuda")
+    if out.dtype == torch.float32:
+        out.fill_(float("nan"))             # every pixel must be written
+    torch.cuda.synchronize()                # (the run may be on another stream)
+    dec.run(lat, w, b, out=out, stream=stream)
     torch.cuda.synchronize()
     info = dec.info()
     dec.close()
-    return out.cpu().numpy(), info
+    got = out.cpu().numpy()
+    if got.dtype == np.float32:
+        assert np.isfinite(got).all(), "pixels left unwritten"
+    return got, info
 
 
 def _strips(H, n=24):
