@@ -454,6 +454,10 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
     const int len0 = first_length(p);
     const StagedWords sw = load_words(p, w0);
     build_code(p, s_tab, len0);
+    if (blockIdx.x == 0 && l == 0) {       // the call's status starts here
+        *p.status = s_tab.valid ? 0 : PIC_HUFF_ERR_TABLE;
+        p.flags[1] = 0x7fffffff;           // first subsequence whose true parse meets no codeword
+    }
     if (!s_tab.valid)
         return;   // uniform
     build_lut(s_tab);
@@ -600,6 +604,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
     const int seg = (nblk + kHuffThreads - 1) / kHuffThreads;
     const int seg_lo = threadIdx.x * seg, seg_hi = seg_lo + seg < nblk ? seg_lo + seg : nblk;
     const int len0 = first_length(p);
+    const int32_t status0 = *p.status;     // the parse kernel's: whether the table is valid
     int32_t count = 0;
     uint32_t mine = 0;                     // the segment's workgroups to repair, while seg <= 32
     for (int g = seg_lo; g < seg_hi; g += 8) {
@@ -617,16 +622,12 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_fix(HuffParams p)
                     mine |= 1u << (g + j - seg_lo);
             }
     }
-    build_code(p, s_tab, len0);
-    if (threadIdx.x == 0) {
-        *p.status = s_tab.valid ? 0 : PIC_HUFF_ERR_TABLE;
-        p.flags[1] = 0x7fffffff;           // first subsequence whose true parse meets no codeword
-    }
-    if (!s_tab.valid)
-        return;   // uniform
+    if (status0 & PIC_HUFF_ERR_TABLE)
+        return;   // uniform: nothing was parsed
     int32_t total;
     const int32_t at = block_sum_incl(count, s_wsum, &total) - count;
-    if (total > 0) {   // uniform
+    if (total > 0) {   // uniform; the tables are needed only to repair
+        build_code(p, s_tab, len0);
         const bool listed = total <= kList && seg <= 32;
         if (listed)
             for (uint32_t b = mine; b; b &= b - 1u)
