@@ -711,6 +711,17 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     const int32_t cnt_t = p.cnt[rec ? t : 0];           // (unused unless rec)
     const uint64_t mask_t = p.mask[rec ? t : 0];
     const int32_t blk_before = p.blk_is_prefix ? p.blk[blockIdx.x] : 0;
+    // the counts of up to 8 x kHuffThreads workgroups before this one, for
+    // the symbols before it (branch-free: an index past them reads entry 0
+    // and is dropped)
+    int32_t pre[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int j = l + u * kHuffThreads;
+        const bool in = !p.blk_is_prefix && j < (int)blockIdx.x;
+        const int32_t v = p.blk[in ? j : 0];
+        pre[u] = in ? v : 0;
+    }
     build_code(p, s_tab, len0);
     if (!s_tab.valid)
         return;   // uniform
@@ -724,8 +735,11 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
     if (p.blk_is_prefix) {
         before = blk_before;
     } else {
-        int32_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int j = l; j < (int)blockIdx.x; j += 8 * kHuffThreads) {
+        int32_t a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            a[u] = pre[u];
+        for (int j = l + 8 * kHuffThreads; j < (int)blockIdx.x; j += 8 * kHuffThreads) {
 #pragma unroll
             for (int u = 0; u < 8; ++u)
                 a[u] += j + u * kHuffThreads < (int)blockIdx.x ? p.blk[j + u * kHuffThreads] : 0;
