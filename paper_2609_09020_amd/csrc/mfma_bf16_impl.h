@@ -300,17 +300,23 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                             d[ob][r] = relu(e[ob][r]);
                 }
 
-                // output layer on the vector ALU (fp32)
+                // output layer on the vector ALU (fp32); a block's four weight
+                // reads are issued before their first use, so one LDS round
+                // trip covers them
                 float o0 = ob0, o1 = ob1, o2 = ob2;
 #pragma unroll
-                for (int ob = 0; ob < NB; ++ob)
+                for (int ob = 0; ob < NB; ++ob) {
+                    f32x4 w3[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        w3[r] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((ob * 4 + r) * 4 + g) * 4]);
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const f32x4 w3 = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((ob * 4 + r) * 4 + g) * 4]);
-                        o0 = __builtin_fmaf(w3[0], d[ob][r], o0);
-                        o1 = __builtin_fmaf(w3[1], d[ob][r], o1);
-                        o2 = __builtin_fmaf(w3[2], d[ob][r], o2);
+                        o0 = __builtin_fmaf(w3[r][0], d[ob][r], o0);
+                        o1 = __builtin_fmaf(w3[r][1], d[ob][r], o1);
+                        o2 = __builtin_fmaf(w3[r][2], d[ob][r], o2);
                     }
+                }
                 const float v = row_sum3(o0, o1, o2);
                 if (g < 3 && tx0 + 16 * cg + col <= tx1)
                     store_out(p, orow + 16 * cg, v);
