@@ -31,6 +31,8 @@ namespace mfma_bf16 {
 using namespace tile;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 template <int NB, int NH, int LPG>
@@ -50,12 +52,13 @@ struct Layout {
 __device__ __forceinline__ u32x2 split_pair(float x0, float x1)
 {
     const unsigned b0 = __float_as_uint(x0), b1 = __float_as_uint(x1);
-    const unsigned hi = (b0 >> 16) | (b1 & 0xffff0000u);
+    // the high halves of b0 and b1, in one byte permute
+    const unsigned hi = __builtin_amdgcn_perm(b1, b0, 0x07060302u);
     const float r0 = x0 - __uint_as_float(b0 & 0xffff0000u);
     const float r1 = x1 - __uint_as_float(b1 & 0xffff0000u);
-    const __bf16 l0 = (__bf16)r0, l1 = (__bf16)r1;
-    const unsigned lo = (unsigned)__builtin_bit_cast(uint16_t, l0) | ((unsigned)__builtin_bit_cast(uint16_t, l1) << 16);
-    return u32x2{hi, lo};
+    // both remainders rounded to bfloat16 by one packed conversion
+    const bf16x2 l = __builtin_convertvector((f32x2{r0, r1}), bf16x2);
+    return u32x2{hi, __builtin_bit_cast(unsigned, l)};
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
