@@ -102,18 +102,15 @@ __device__ __forceinline__ void build_b(const float (&v)[Q], float sc, u32x4 (&b
 {
     constexpr int T = (Q + 1) / 2;
     unsigned reg[4 * ksteps(Q)];
-    _Float16 hi[2 * T];
-#pragma unroll
-    for (int q = 0; q < 2 * T; ++q)
-        hi[q] = q < Q ? (_Float16)(v[q] * sc) : (_Float16)0.0f;
-#pragma unroll
-    for (int t = 0; t < T; ++t)                // (hi, hi) pairs
-        reg[Q + t] = __builtin_bit_cast(unsigned, f16x2{hi[2 * t], hi[2 * t + 1]});
 #pragma unroll
     for (int q = 0; q < Q; ++q) {              // (hi, lo)
-        const _Float16 lo = (_Float16)__builtin_fmaf(v[q], sc, -(float)hi[q]);
-        reg[q] = __builtin_bit_cast(unsigned, f16x2{hi[q], lo});
+        const _Float16 hi = (_Float16)(v[q] * sc);
+        const _Float16 lo = (_Float16)__builtin_fmaf(v[q], sc, -(float)hi);
+        reg[q] = __builtin_bit_cast(unsigned, f16x2{hi, lo});
     }
+#pragma unroll
+    for (int t = 0; t < T; ++t)                // (hi, hi) pairs: the low halves of two (hi, lo) registers
+        reg[Q + t] = __builtin_amdgcn_perm(2 * t + 1 < Q ? reg[2 * t + 1] : 0u, reg[2 * t], 0x05040100u);
 #pragma unroll
     for (int k = Q + T; k < 4 * ksteps(Q); ++k)
         reg[k] = 0u;
