@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     static_assert(NS % kZprThreads == 0, "staging must divide evenly");
     __shared__ int32_t s_sym[NS];
     __shared__ int32_t s_cex[NS];                  // coefficients produced by the staged symbols before
-    __shared__ int16_t s_rid[NS];                  // chunk markers before the symbol: its block
+    __shared__ uint16_t s_code[NS];                // where a coefficient value goes: block * 64 + tile word
     __shared__ int32_t s_pos[CH + 1];              // [0]: marker before block 0; [1 + r]: block r's marker
     __shared__ __attribute__((aligned(16))) float s_blk[kGroups * kTile];   // tiles: S, then T in place
     __shared__ uint8_t s_zz[64];
@@ -290,16 +290,16 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     // symbol its block (markers before it) and the coefficients produced
     // before it, so a symbol's place in its block is a difference of two
     // prefixes -- Alg. 1's running offset without a serial walk.
-    int c[SPS];
+    int32_t sv[SPS], c[SPS], cp[SPS], rr[SPS];
     uint32_t mflags = 0;
     int32_t csum = 0, nm = 0;
 #pragma unroll
     for (int j = 0; j < SPS; ++j) {
         const int i = t * SPS + j;
-        const int32_t s = s_sym[i];
+        sv[j] = s_sym[i];
         const int k = i - kHalo;
-        const bool mk = k >= 0 && cs + k < p.n && s == eob;
-        c[j] = zpr_coeffs(s, eob);
+        const bool mk = k >= 0 && cs + k < p.n && sv[j] == eob;
+        c[j] = zpr_coeffs(sv[j], eob);
         csum += c[j];
         nm += mk ? 1 : 0;
         mflags |= mk ? 1u << j : 0u;
@@ -312,7 +312,8 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     for (int j = 0; j < SPS; ++j) {
         const int i = t * SPS + j;
         s_cex[i] = cpre;
-        s_rid[i] = (int16_t)mpre;
+        cp[j] = cpre;
+        rr[j] = mpre;
         cpre += c[j];
         if (mflags >> j & 1u)
             s_pos[1 + mpre++] = i;
@@ -338,39 +339,60 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
         if (lane == 0)
             s_pos[0] = prev;
     }
+    __syncthreads();
 
-    // Windows of kGroups blocks: zero the tiles, scatter the window's
-    // coefficient values through the zigzag table (any thread, any block),
-    // then eight lanes per block transform and store it.
+    // Each symbol's destination, once: block r (< m, one the stream has)
+    // begins after s_pos[r], and a coefficient value lands at its place in
+    // the block through the zigzag table.  Symbols outside the chunk's blocks
+    // and markers get no slot; a symbol above the marker is flagged and
+    // skipped, as Alg. 1 has no code for it; a block of more than 64 symbols
+    // or coefficients is flagged once any of its symbols passes 64.  The
+    // code fits 16 bits: a slot's block holds a symbol of the chunk, so it
+    // is at most CH - 2.
+    const int p0 = s_pos[0];
+    int err = 0;
+#pragma unroll
+    for (int j = 0; j < SPS; ++j) {
+        const int i = t * SPS + j;
+        const int r = rr[j];
+        uint32_t code = 0xffffu;
+        if (r < m && i > p0 && g0 + r < p.expected && sv[j] != eob) {
+            if (sv[j] > eob) {
+                err |= PIC_ZPR_ERR_SYMBOL;
+            } else {
+                const int begin = s_pos[r] + 1;
+                const int pos = cp[j] - s_cex[begin];
+                if (i - begin >= 64 || pos + c[j] > 64)
+                    err |= PIC_ZPR_ERR_OVERFLOW;
+                if (sv[j] <= eob - 17 && pos < 64)
+                    code = (uint32_t)r << 6 | s_zz[pos];
+            }
+        }
+        s_code[i] = (uint16_t)code;
+    }
+
+    // Windows of kGroups blocks: zero the tiles, write the window's
+    // coefficient values into their slots (any thread, any block), then
+    // eight lanes per block transform and store it.
     const int grp = t >> 3, gl = t & 7;
     float *blk = s_blk + grp * kTile;
     const int32_t img0 = g0 / p.blocks_per_image;
     const int32_t j0 = g0 - img0 * p.blocks_per_image;
-    int err = 0;
     for (int r0 = 0; r0 < m; r0 += kGroups) {
         reinterpret_cast<float4 *>(blk + gl * 8)[0] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         reinterpret_cast<float4 *>(blk + gl * 8)[1] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        __syncthreads();   // tiles zeroed (and s_pos[0] written, first round)
+        __syncthreads();   // tiles zeroed (and the slots written, first round)
         const int rend = r0 + kGroups < m ? r0 + kGroups : m;
         const int lo = s_pos[r0] + 1, hi = s_pos[rend];
         for (int i = lo + t; i < hi; i += kZprThreads) {
+            const uint32_t code = s_code[i];
             const int32_t s = s_sym[i];
-            const int r = s_rid[i];
-            if (g0 + r >= p.expected || s == eob)
-                continue;                            // a block past the stream's last, or a marker
-            if (s > eob) {
-                err |= PIC_ZPR_ERR_SYMBOL;           // skipped, as Alg. 1 has no code for it
-                continue;
-            }
-            if (s <= eob - 17) {                     // a coefficient value
-                const int pos = s_cex[i] - s_cex[s_pos[r] + 1];
-                if (pos < 64) {
-                    float *tile = s_blk + (r - r0) * kTile;
-                    if (COEFF)
-                        reinterpret_cast<int32_t *>(tile)[s_zz[pos]] = s;
-                    else
-                        tile[s_zz[pos]] = (float)s;
-                }
+            if (code != 0xffffu) {
+                float *word = s_blk + ((int)(code >> 6) - r0) * kTile + (code & 63u);
+                if (COEFF)
+                    *reinterpret_cast<int32_t *>(word) = s;
+                else
+                    *word = (float)s;
             }
         }
         __syncthreads();   // the window's tiles are complete
@@ -378,11 +400,6 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
         const int r = r0 + grp;
         const int32_t g = g0 + r;
         if (r < m && g < p.expected) {               // uniform over the 8 lanes of a block
-            if (gl == 0) {
-                const int end = s_pos[1 + r], begin = s_pos[r] + 1;
-                if (end - begin > 64 || s_cex[end] - s_cex[begin] > 64)
-                    err |= PIC_ZPR_ERR_OVERFLOW;
-            }
             if (COEFF) {
                 const int4 *src = reinterpret_cast<const int4 *>(blk + gl * 8);
                 int4 *dst = reinterpret_cast<int4 *>(p.coeffs + (int64_t)g * 64 + gl * 8);
