@@ -410,7 +410,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU (the decoder has no multi-GPU "
+        print("bench.py: runs on exactly one GPU (the decoder has no multi-GPU "
               "path); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 

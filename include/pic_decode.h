@@ -57,7 +57,7 @@ typedef struct pic_decoder pic_decoder;
 typedef enum pic_status {
     PIC_OK = 0,
     PIC_E_INVALID = 1,      /* an argument is out of range or a pointer is NULL   */
-    PIC_E_UNSUPPORTED = 2,  /* valid request this build does not handle           */
+    PIC_E_UNSUPPORTED = 2,  /* valid request the library does not handle          */
     PIC_E_NODEVICE = 3,     /* no HIP device, or the current device is not gfx950 */
     PIC_E_HIP = 4,          /* the HIP runtime reported an error (launch failure) */
     PIC_E_NOMEM = 5         /* host allocation of the handle failed               */
