@@ -248,6 +248,17 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     const int t = threadIdx.x, lane = t & 63;
     const int64_t cs = (int64_t)blockIdx.x * CH;
     const int32_t eob = p.eob;
+    // Stage [cs - kHalo, cs + CH).  Positions before the stream act as markers
+    // (the first block starts at 0); positions past its end are never markers
+    // and never inside a block.  The loads go out first and land in LDS after
+    // the prefix below, so the two round trips overlap.
+    int32_t staged[SPS];
+#pragma unroll
+    for (int u = 0; u < SPS; ++u) {
+        const int64_t gi = cs - kHalo + t + u * kZprThreads;
+        staged[u] = gi < 0 ? eob : (gi < p.n ? p.sym[gi] : 0);
+    }
+
     // Blocks whose markers precede the chunk: the scan kernel's prefix, or the
     // sum of the earlier chunks' counts (L2-resident; eight independent loads
     // in flight per thread).
@@ -266,13 +277,9 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
         (void)block_inclusive_sum(part, s_wsum, &g0);
     }
 
-    // Stage [cs - kHalo, cs + CH).  Positions before the stream act as markers
-    // (the first block starts at 0); positions past its end are never markers
-    // and never inside a block.
-    for (int i = t; i < NS; i += kZprThreads) {
-        const int64_t gi = cs - kHalo + i;
-        s_sym[i] = gi < 0 ? eob : (gi < p.n ? p.sym[gi] : 0);
-    }
+#pragma unroll
+    for (int u = 0; u < SPS; ++u)
+        s_sym[t + u * kZprThreads] = staged[u];
     if (t < 64)
         s_zz[t] = kZigzag[t];
     if (!COEFF && t < p.L) {
