@@ -233,10 +233,12 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     constexpr int NS = kHalo + CH;                 // staged symbols
     constexpr int SPS = NS / kZprThreads;          // per thread, consecutive
     static_assert(NS % kZprThreads == 0, "staging must divide evenly");
+    static_assert(NS * 16 < 32768, "coefficient prefixes and positions fit 16 bits");
     __shared__ int32_t s_sym[NS];
-    __shared__ int32_t s_cex[NS];                  // coefficients produced by the staged symbols before
+    __shared__ uint16_t s_cex[NS];                 // coefficients produced by the staged symbols before
+                                                   // (at most 16 per symbol: < 2^15)
     __shared__ uint16_t s_code[NS];                // where a coefficient value goes: block * 64 + tile word
-    __shared__ int32_t s_pos[CH + 1];              // [0]: marker before block 0; [1 + r]: block r's marker
+    __shared__ int16_t s_pos[CH + 1];              // [0]: marker before block 0; [1 + r]: block r's marker
     __shared__ __attribute__((aligned(16))) float s_blk[kGroups * kTile];   // tiles: S, then T in place
     __shared__ uint8_t s_zz[64];
     __shared__ int4 s_geo[PIC_MAX_LEVELS];         // stream level i: {h, w, pw | k << 16, ceil(2^k / pw)}
@@ -318,12 +320,12 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
 #pragma unroll
     for (int j = 0; j < SPS; ++j) {
         const int i = t * SPS + j;
-        s_cex[i] = cpre;
+        s_cex[i] = (uint16_t)cpre;
         cp[j] = cpre;
         rr[j] = mpre;
         cpre += c[j];
         if (mflags >> j & 1u)
-            s_pos[1 + mpre++] = i;
+            s_pos[1 + mpre++] = (int16_t)i;
     }
     __syncthreads();
     if (t == 0 && blockIdx.x == (unsigned)p.nchunks - 1 &&
@@ -344,7 +346,7 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
         else
             prev = s_sym[f - 65] == eob ? f - 65 : f - 66;
         if (lane == 0)
-            s_pos[0] = prev;
+            s_pos[0] = (int16_t)prev;
     }
     __syncthreads();
 
