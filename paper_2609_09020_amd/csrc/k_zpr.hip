@@ -236,8 +236,9 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     static_assert(NS * 16 < 32768, "coefficient prefixes and positions fit 16 bits");
     __shared__ int32_t s_sym[NS];
     __shared__ uint16_t s_cex[NS];                 // coefficients produced by the staged symbols before
-                                                   // (at most 16 per symbol: < 2^15)
-    __shared__ uint16_t s_code[NS];                // where a coefficient value goes: block * 64 + tile word
+                                                   // (at most 16 per symbol: < 2^15); once read, where
+                                                   // a coefficient value goes: block * 64 + tile word
+    uint16_t *const s_code = s_cex;
     __shared__ int16_t s_pos[CH + 1];              // [0]: marker before block 0; [1 + r]: block r's marker
     __shared__ __attribute__((aligned(16))) float s_blk[kGroups * kTile];   // tiles: S, then T in place
     __shared__ uint8_t s_zz[64];
@@ -360,11 +361,12 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
     // is at most CH - 2.
     const int p0 = s_pos[0];
     int err = 0;
+    uint32_t code[SPS];
 #pragma unroll
     for (int j = 0; j < SPS; ++j) {
         const int i = t * SPS + j;
         const int r = rr[j];
-        uint32_t code = 0xffffu;
+        code[j] = 0xffffu;
         if (r < m && i > p0 && g0 + r < p.expected && sv[j] != eob) {
             if (sv[j] > eob) {
                 err |= PIC_ZPR_ERR_SYMBOL;
@@ -374,11 +376,14 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
                 if (i - begin >= 64 || pos + c[j] > 64)
                     err |= PIC_ZPR_ERR_OVERFLOW;
                 if (sv[j] <= eob - 17 && pos < 64)
-                    code = (uint32_t)r << 6 | s_zz[pos];
+                    code[j] = (uint32_t)r << 6 | s_zz[pos];
             }
         }
-        s_code[i] = (uint16_t)code;
     }
+    __syncthreads();   // every prefix is read: the slots take their place
+#pragma unroll
+    for (int j = 0; j < SPS; ++j)
+        s_code[t * SPS + j] = (uint16_t)code[j];
 
     // Windows of kGroups blocks: zero the tiles, write the window's
     // coefficient values into their slots (any thread, any block), then
