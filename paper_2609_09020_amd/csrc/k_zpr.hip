@@ -446,10 +446,12 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_expand(ZprParams p)
                 img += d;
                 j -= d * p.blocks_per_image;
             }
+            // The level: the table runs past the last level with blocks no
+            // image has, so every entry can be compared.
             int lv = 0;
 #pragma unroll
             for (int i = 1; i < PIC_MAX_LEVELS; ++i)
-                lv += (i < p.L && j >= p.first[i]) ? 1 : 0;
+                lv += j >= p.first[i] ? 1 : 0;
             const int4 geo = s_geo[lv];
             float *base = s_lat[lv];
             // q / pw as (q * ceil(2^k / pw)) >> k, k = 24 + ceil(log2 pw): exact

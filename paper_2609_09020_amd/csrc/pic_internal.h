@@ -103,7 +103,8 @@ struct ZprParams {
     int32_t counts_are_prefix;      // 1: the scan kernel ran (long streams)
     int32_t *status;                // PIC_ZPR_ERR_* bits of the run
     // levels in stream order, i = 0 the coarsest (level k = L - 1 - i)
-    int32_t first[PIC_MAX_LEVELS + 1];   // first block of stream level i inside an image
+    int32_t first[PIC_MAX_LEVELS + 1];   // first block of stream level i inside an image;
+                                         // [L]: blocks per image; INT32_MAX past it
     int32_t hk[PIC_MAX_LEVELS];
     int32_t wk[PIC_MAX_LEVELS];
     int32_t pw[PIC_MAX_LEVELS];          // patches per row

@@ -86,8 +86,8 @@ pic_status prepare(const pic_zpr *h, int32_t batch, const int32_t *symbols, int6
     p.counts = h->d_counts;
     p.counts_are_prefix = p.nchunks > kPrefixInKernelMax;
     p.status = status;
-    for (int i = 0; i <= p.L; ++i)
-        p.first[i] = h->first[i];
+    for (int i = 0; i <= PIC_MAX_LEVELS; ++i)   // past the end: no block reaches these
+        p.first[i] = i <= p.L ? h->first[i] : INT32_MAX;
     for (int i = 0; i < p.L; ++i) {
         p.hk[i] = h->hk[i];
         p.wk[i] = h->wk[i];
