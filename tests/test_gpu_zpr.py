@@ -229,6 +229,49 @@ def test_malformed_streams(orc, name, shape):
         assert np.allclose(got[k], want[k], rtol=0, atol=1e-3), f"level {k}"
 
 
+def _replace_blocks(symbols, eob, body, every):
+    """The stream with every `every`-th block's symbols replaced by `body`."""
+    out, cur, k = [], [], 0
+    for t in symbols:
+        if t != eob:
+            cur.append(t)
+            continue
+        out += (body if k % every == every - 1 else cur) + [eob]
+        cur, k = [], k + 1
+    return out + cur
+
+
+# block bodies at the 64-symbol / 64-coefficient limits (Alg. 1: a block
+# holds 64 coefficients): exactly 64 is a whole block, 65 is flagged
+LIMIT_BODIES = {
+    "values_64": (lambda eob: [((v * 7) % 23) - 11 or 1 for v in range(64)], 0),
+    "runs_64": (lambda eob: [eob - 1] * 4, 0),
+    "runs_and_values_64": (lambda eob: [5, eob - 1, -3] + [eob - 2] * 3 + [4], 0),
+    "values_65": (lambda eob: [2] * 65, D.PIC_ZPR_ERR_OVERFLOW),
+    "runs_65": (lambda eob: [eob - 1] * 4 + [1], D.PIC_ZPR_ERR_OVERFLOW),
+}
+
+
+@pytest.mark.parametrize("shape", MALFORMED_SHAPES, ids=["short", "long"])
+@pytest.mark.parametrize("name", list(LIMIT_BODIES))
+def test_blocks_at_the_length_limit(orc, name, shape):
+    H, W, L, batch = shape
+    s = synth.make_zpr_stream(H, W, L, batch, seed=11)
+    body_of, flag = LIMIT_BODIES[name]
+    body = body_of(s.eob)
+    assert all(t != s.eob for t in body)
+    stream = np.array(_replace_blocks(s.symbols, s.eob, body, every=13), np.int32)
+    _print_case("limit", name, stream.size)
+    fill = -77.25
+    got, st = _gpu_decode(H, W, L, batch, stream, s.eob, fill=fill)
+    want, err = orc.zpr_decode(stream, s.eob, H, W, L, batch, fill=fill)
+    assert err == flag and st == err
+    if flag:
+        return   # the values of an over-long block are unspecified; the flag is the contract
+    for k in range(L):
+        assert np.allclose(got[k], want[k], rtol=0, atol=1e-3), f"level {k}"
+
+
 def test_full_size_batch_sampled(orc):
     # the launch the benchmark times (768x512, 7 levels, 64 images), every
     # sample compared for three images decoded by the oracle one by one
