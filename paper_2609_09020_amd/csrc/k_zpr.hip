@@ -111,15 +111,26 @@ __global__ __launch_bounds__(kZprThreads) void k_zpr_count(ZprParams p)
     __shared__ int32_t s_wsum[kWaves];
     const int t = threadIdx.x;
     const int64_t cs = (int64_t)blockIdx.x * CH;
-    int32_t mine = 0;
+    int32_t v[SPT];
 #pragma unroll
     for (int j = 0; j < SPT; ++j) {
         const int64_t i = cs + j * kZprThreads + t;
-        mine += (i < p.n && p.sym[i] == p.eob) ? 1 : 0;
+        v[j] = i < p.n ? p.sym[i] : ~p.eob;
     }
-    int32_t tot;
-    (void)block_inclusive_sum(mine, s_wsum, &tot);
+    // each wave's markers: one ballot per row of symbols, counted on the
+    // scalar unit
+    int32_t mine = 0;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j)
+        mine += __popcll(__ballot(v[j] == p.eob));
+    if ((t & 63) == 0)
+        s_wsum[t >> 6] = mine;
+    __syncthreads();
     if (t == 0) {
+        int32_t tot = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w)
+            tot += s_wsum[w];
         p.counts[blockIdx.x] = tot;
         if (blockIdx.x == 0)
             *p.status = 0;     // the decoding kernel ors its findings into it
