@@ -24,14 +24,15 @@
 //                 block's symbols start after the previous marker, found in
 //                 the chunk or, for the first block, within the 65 staged
 //                 symbols before it (a block of 64 symbols plus the preceding
-//                 marker).  Blocks are then decoded in windows of 32: the
-//                 tiles are zeroed, every coefficient value of the window is
-//                 written through the zigzag table into its block's 8x8
-//                 tile, and eight lanes per block run the separable inverse
-//                 DCT (rows, an LDS transpose, columns; a factored 8-point
-//                 transform with compile-time constants) and write the
-//                 block's patch of its latent grid, cropped at the grid's
-//                 edge.
+//                 marker).  Each coefficient value's slot (its block and,
+//                 through the zigzag table, its word of the block's 8x8
+//                 tile) is found once.  Blocks are then decoded in windows
+//                 of 32: the tiles are zeroed, every coefficient value of the
+//                 window is written to its slot, and eight lanes per block
+//                 run the separable inverse DCT (rows, an LDS transpose,
+//                 columns; a factored 8-point transform with compile-time
+//                 constants) and write the block's patch of its latent grid,
+//                 cropped at the grid's edge.
 //
 // Memory traffic: the stream read by both kernels (plus the expand kernel's
 // 256-symbol halos) and the pyramid written once; the HBM floor of the step
