@@ -17,8 +17,8 @@ int hidden_blocks(int nl, const int32_t *widths)
 int hidden_values(int nl, const int32_t *widths)
 {
     int m = 1;
-    for (int l = 1; l < nl - 1; ++l)     // inputs of the hidden layers
-        m = widths[l] > m ? widths[l] : m;
+    for (int l = 1; l < nl; ++l)     // every hidden width: the inputs of the hidden
+        m = widths[l] > m ? widths[l] : m;   // layers and of the output layer
     return (m + 3) / 4;
 }
 

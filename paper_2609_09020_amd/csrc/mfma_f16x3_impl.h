@@ -498,8 +498,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
 
 int hidden_blocks(int nl, const int32_t *widths);
 
-// Values per lane group of the hidden layers' inputs: ceil(width / 4) of the
-// widest hidden input.
+// Values per lane group of the hidden activations: ceil(width / 4) of the
+// widest hidden layer (the last one feeds the output layer, so it counts too).
 int hidden_values(int nl, const int32_t *widths);
 
 template <int NB, int NH, int LS, int KSH>
