@@ -91,7 +91,7 @@ typedef enum pic_variant {
 enum {
     PIC_MAX_LEVELS = 12,    /* L                                                  */
     PIC_MAX_LAYERS = 8,     /* linear layers                                      */
-    PIC_MAX_WIDTH = 64,     /* hidden width                                       */
+    PIC_MAX_WIDTH = 128,    /* hidden width                                       */
     PIC_MAX_BATCH = 65535   /* images per call                                    */
 };
 

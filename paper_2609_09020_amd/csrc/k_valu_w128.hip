@@ -1,0 +1,11 @@
+// The reference family's instance for hidden widths up to 128 (levels padded to
+// 12); one translation unit of its own because it is large.
+#include "valu_impl.h"
+
+namespace pic {
+namespace valu {
+
+hipError_t launch_wide128(const DecodeParams &p, hipStream_t s) { return launch_t<12, 128>(p, s); }
+
+}  // namespace valu
+}  // namespace pic

@@ -23,7 +23,7 @@ LIB_PATH = os.path.join(PKG, "libpic_decode.so")
 PIC_OK, PIC_E_INVALID, PIC_E_UNSUPPORTED, PIC_E_NODEVICE, PIC_E_HIP, PIC_E_NOMEM = range(6)
 PIC_F32, PIC_BF16, PIC_U8 = 0, 1, 2
 PIC_VARIANT_AUTO, PIC_VARIANT_VALU, PIC_VARIANT_MFMA_F32, PIC_VARIANT_MFMA_BF16, PIC_VARIANT_MFMA_F16X3 = range(5)
-PIC_MAX_LEVELS, PIC_MAX_LAYERS, PIC_MAX_WIDTH, PIC_MAX_BATCH = 12, 8, 64, 65535
+PIC_MAX_LEVELS, PIC_MAX_LAYERS, PIC_MAX_WIDTH, PIC_MAX_BATCH = 12, 8, 128, 65535
 PIC_FLAG_NO_CLAMP = 1
 
 VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,

@@ -91,7 +91,7 @@ def _gpu_present():
     dict(height=0), dict(width=-1), dict(widths=(4, 16, 16, 4)),
     dict(widths=(3, 16, 16, 3), _raw={"num_levels": 4}), dict(_raw={"num_layers": 0}),
     dict(_raw={"num_layers": 9}),
-    dict(widths=(4, 65, 3)), dict(widths=(4, 0, 3)), dict(weight_dtype=2), dict(out_dtype=1),
+    dict(widths=(4, 129, 3)), dict(widths=(4, 16, 129, 3)), dict(widths=(4, 0, 3)), dict(weight_dtype=2), dict(out_dtype=1),
     dict(flags=2), dict(flags=D.PIC_FLAG_NO_CLAMP, out_dtype=D.PIC_U8), dict(max_batch=0),
     dict(max_batch=70000), dict(variant=9), dict(variant=5), dict(height=65536, width=32768),
     dict(widths=(13,) + (16,) * 2 + (3,)),
@@ -115,6 +115,22 @@ def test_unsupported_combinations():
     assert _create_status(variant=D.PIC_VARIANT_MFMA_F16X3, weight_dtype=D.PIC_BF16) == D.PIC_E_UNSUPPORTED
     # the matrix-core families take 2 to 4 linear layers
     assert _create_status(variant=D.PIC_VARIANT_MFMA_F16X3, widths=(4, 3)) == D.PIC_E_UNSUPPORTED
+    # ... and hidden widths up to 64 (four 16-neuron blocks); wider nets run on
+    # the reference family, which AUTO then picks
+    for v in (D.PIC_VARIANT_MFMA_F32, D.PIC_VARIANT_MFMA_F16X3):
+        for widths in ((4, 65, 3), (8, 64, 96, 3), (8, 128, 128, 3)):
+            assert _create_status(variant=v, widths=widths) == D.PIC_E_UNSUPPORTED
+    assert _create_status(variant=D.PIC_VARIANT_MFMA_BF16, weight_dtype=D.PIC_BF16,
+                          widths=(8, 128, 3)) == D.PIC_E_UNSUPPORTED
+
+
+@pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
+def test_widest_descriptors_pass_validation():
+    # the largest hidden width, level count and depth are valid descriptors:
+    # validation passes, and the CPU host then has no device
+    assert _create_status(widths=(4, 128, 3)) == D.PIC_E_NODEVICE
+    assert _create_status(widths=(12,) + (128,) * 7 + (3,)) == D.PIC_E_NODEVICE
+    assert _create_status(widths=(12,) + (128,) * 7 + (3,), variant=D.PIC_VARIANT_VALU) == D.PIC_E_NODEVICE
 
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
