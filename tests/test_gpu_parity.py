@@ -12,8 +12,9 @@ move 255 c + 1/2 across an integer only from inside the band):
   * reference family raw output: equal, value for value, to the binary32
     model for any inputs (same operations in the same order).
 Full-size workloads run on the GPU at full size in the launch configuration
-the benchmark times; the oracle checks sampled images and row strips
-(top edge, middle, bottom edge) of them.
+the benchmark times, and every pixel of every image is compared with the
+oracle (which runs on all host cores; one workload's oracle results are kept
+while its families and output kinds are checked, then dropped).
 """
 import numpy as np
 import pytest
@@ -27,6 +28,7 @@ pytestmark = pytest.mark.gpu
 
 TOL = 1e-5
 U8_BAND = 255 * TOL
+BF16_TOL = 4e-3
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -69,94 +71,110 @@ def gpu_decode(inp, variant="auto", out_dtype="f32", clamp=True, shared=False, s
     return got, info
 
 
-def _strips(H, n=24):
-    if H <= 3 * n:
-        return [(0, H)]
-    m = H // 2
-    return [(0, n), (m - n // 2, m + n // 2), (H - n, H)]
-
-
 def _check_float(got, ref, raw, what):
-    if raw:
-        err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
-    else:
-        err = np.max(np.abs(got - ref))
-    print(f"PARITY {what}: max err {err:.3e}", flush=True)
+    """Max error over the whole output, image by image (bounded temporaries)."""
+    err = 0.0
+    for b in range(got.shape[0]):
+        g, r = got[b], ref[b]
+        if raw:
+            e = np.max(np.abs(g - r) / np.maximum(1.0, np.abs(r)))
+        else:
+            e = np.max(np.abs(g - r))
+        err = max(err, float(e))
+    print(f"PARITY {what}: max err {err:.3e} over {got.size} values", flush=True)
     assert err <= TOL, what
 
 
 def _check_u8_band(got, ref_clamped, ref_u8, what):
-    t = 255.0 * ref_clamped + 0.5
-    safe = np.abs(t - np.round(t)) > U8_BAND
-    diff = got.astype(np.int32) - ref_u8.astype(np.int32)
-    n_band = int(np.count_nonzero(diff[~safe]))
+    n_band = n_band_samples = 0
+    for b in range(got.shape[0]):
+        t = 255.0 * ref_clamped[b] + 0.5
+        safe = np.abs(t - np.round(t)) > U8_BAND
+        diff = got[b].astype(np.int32) - ref_u8[b].astype(np.int32)
+        n_band += int(np.count_nonzero(diff[~safe]))
+        n_band_samples += int(np.count_nonzero(~safe))
+        assert np.array_equal(got[b][safe], ref_u8[b][safe]), f"{what} image {b}"
+        assert np.all(np.abs(diff) <= 1), f"{what} image {b}"
     print(f"PARITY {what}: u8 codes differing inside the rounding band: {n_band} "
-          f"of {int(np.count_nonzero(~safe))} band samples", flush=True)
-    assert np.array_equal(got[safe], ref_u8[safe]), what
-    assert np.all(np.abs(diff) <= 1), what
+          f"of {n_band_samples} band samples; {got.size} codes", flush=True)
+
+
+class _Workload:
+    """The inputs and whole-output oracle results of one workload at a time."""
+    name = None
+    inp = None
+    refs = {}
+
+    @classmethod
+    def get(cls, name):
+        if cls.name != name:
+            cls.name, cls.inp, cls.refs = None, None, {}
+            cls.inp = synth.workload_inputs(synth.WORKLOADS[name])
+            cls.name = name
+        return cls.inp
+
+    @classmethod
+    def ref(cls, out, precision="f64"):
+        key = (out, precision)
+        if key not in cls.refs:
+            cls.refs[key] = oracle.decode_inputs(cls.inp, out=out, precision=precision)
+        return cls.refs[key]
 
 
 FULL = ["pic64", "kodak768", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k", "kodak768_paper"]
 F32_VARIANTS = ["valu", "mfma_f32", "mfma_f16x3"]
+KINDS = ["clamped", "raw", "u8"]
+# every (workload, kind, family), grouped by workload so its oracle results
+# are computed once
+WORKLOAD_CASES = [(n, k, v) for n in FULL for k in KINDS for v in F32_VARIANTS] + \
+                 [("uhd4k_bf16", k, "mfma_bf16") for k in KINDS]
 
 
-def _sample_images(batch):
-    return sorted({0, batch // 2, batch - 1}) if batch > 1 else [0]
-
-
-@pytest.mark.parametrize("variant", F32_VARIANTS)
-@pytest.mark.parametrize("name", FULL)
-def test_workload_fp32_clamped(name, variant):
-    wl = synth.WORKLOADS[name]
-    inp = synth.workload_inputs(wl)
-    got, info = gpu_decode(inp, variant=variant)
+@pytest.mark.parametrize("case", WORKLOAD_CASES, ids=["-".join(c) for c in WORKLOAD_CASES])
+def test_workload_whole_output(case):
+    name, kind, variant = case
+    inp = _Workload.get(name)
+    print(f"case: {name} {kind} {variant}", flush=True)
+    if kind == "u8":
+        got, info = gpu_decode(inp, variant=variant, out_dtype="u8")
+    else:
+        got, info = gpu_decode(inp, variant=variant, clamp=(kind == "clamped"))
     assert info["variant"] == variant
-    for b in _sample_images(inp.batch):
-        for rows in _strips(wl.height):
-            ref = oracle.decode_inputs(inp, out="clamped", batch_slice=slice(b, b + 1), rows=rows)
-            _check_float(got[b:b + 1, :, rows[0]:rows[1]], ref, False,
-                         f"{name} {variant} clamped img{b} rows{rows}")
-
-
-@pytest.mark.parametrize("variant", F32_VARIANTS)
-@pytest.mark.parametrize("name", ["pic64", "kodak768", "clic2048", "uhd4k"])
-def test_workload_raw(name, variant):
-    wl = synth.WORKLOADS[name]
-    inp = synth.workload_inputs(wl)
-    got, _ = gpu_decode(inp, variant=variant, clamp=False)
-    for rows in _strips(wl.height):
-        ref = oracle.decode_inputs(inp, out="raw", rows=rows)
-        _check_float(got[:, :, rows[0]:rows[1]], ref, True, f"{name} {variant} raw rows{rows}")
-
-
-@pytest.mark.parametrize("name", ["pic64", "kodak768", "kodak768_b64", "clic2048", "uhd4k"])
-def test_workload_u8_reference_bit_exact(name):
-    wl = synth.WORKLOADS[name]
-    inp = synth.workload_inputs(wl)
-    got, _ = gpu_decode(inp, variant="valu", out_dtype="u8")
-    for b in _sample_images(inp.batch):
-        for rows in _strips(wl.height):
-            ref = oracle.decode_inputs(inp, out="u8", precision="f32", batch_slice=slice(b, b + 1),
-                                       rows=rows)
-            sub = got[b:b + 1, :, rows[0]:rows[1]]
-            n = int(np.count_nonzero(sub != ref))
-            print(f"PARITY {name} valu u8 img{b} rows{rows}: {n} codes differ", flush=True)
+    what = f"{name} {variant} {kind}"
+    if variant == "mfma_bf16":
+        # 4e-3 against the oracle fed the same bf16 weights
+        if kind == "u8":
+            # an error within 4e-3 of c moves the code by at most 2
+            refc = _Workload.ref("clamped")
+            n = 0
+            for b in range(got.shape[0]):
+                d = np.abs(got[b].astype(np.int32) - np.floor(255 * refc[b] + 0.5).astype(np.int32))
+                n = max(n, int(d.max()))
+            print(f"PARITY {what}: max code difference {n}", flush=True)
+            assert n <= 2
+            return
+        ref = _Workload.ref(kind)
+        err = 0.0
+        for b in range(got.shape[0]):
+            d = np.abs(got[b] - ref[b])
+            if kind == "raw":
+                d = d / np.maximum(1.0, np.abs(ref[b]))
+            err = max(err, float(d.max()))
+        print(f"PARITY {what}: max err {err:.3e} over {got.size} values", flush=True)
+        assert err <= BF16_TOL
+        return
+    if kind == "u8":
+        if variant == "valu":
+            # the reference family takes the 8-bit decision in the oracle's
+            # binary32 model's precision and order: every code equal
+            ref = _Workload.ref("u8", "f32")
+            n = int(np.count_nonzero(got != ref))
+            print(f"PARITY {what}: {n} of {got.size} codes differ from the binary32 model", flush=True)
             assert n == 0
-
-
-@pytest.mark.parametrize("variant", ["mfma_f32", "mfma_f16x3"])
-@pytest.mark.parametrize("name", ["pic64", "kodak768", "kodak768_b64", "clic2048", "uhd4k"])
-def test_workload_u8_mfma_band(name, variant):
-    wl = synth.WORKLOADS[name]
-    inp = synth.workload_inputs(wl)
-    got, _ = gpu_decode(inp, variant=variant, out_dtype="u8")
-    for b in _sample_images(inp.batch):
-        for rows in _strips(wl.height):
-            kw = dict(batch_slice=slice(b, b + 1), rows=rows)
-            refc = oracle.decode_inputs(inp, out="clamped", **kw)
-            refq = oracle.decode_inputs(inp, out="u8", **kw)
-            _check_u8_band(got[b:b + 1, :, rows[0]:rows[1]], refc, refq,
-                           f"{name} {variant} img{b} rows{rows}")
+        else:
+            _check_u8_band(got, _Workload.ref("clamped"), _Workload.ref("u8"), what)
+        return
+    _check_float(got, _Workload.ref(kind), kind == "raw", what)
 
 
 # ------------------------------------------------------------------ fuzz
@@ -189,6 +207,18 @@ EDGE_CASES = [
     (20, 30, (8, 16, 16, 16, 3), 2, 10, False),  # the paper's 4-layer width-16 shape
     (25, 31, (5, 1, 3), 1, 11, False),
     (7, 200, (6, 40, 3), 1, 12, False),
+    # the last hidden layer wider than the earlier ones, in the K-step count
+    # of 33..40-wide nets and beyond it
+    (30, 70, (7, 40, 48, 3), 2, 13, False),
+    (33, 65, (4, 8, 41, 3), 1, 14, False),
+    (17, 90, (5, 40, 40, 44, 3), 1, 15, False),
+    (21, 40, (7, 33, 47, 3), 1, 16, True),
+    # hidden widths past the matrix-core families (four 16-neuron blocks):
+    # the reference family decodes them, the others report them unsupported
+    (19, 37, (7, 65, 3), 1, 17, False),
+    (23, 29, (8, 96, 96, 3), 2, 18, False),
+    (13, 70, (12, 128, 128, 3), 1, 19, False),
+    (9, 33, (3, 128, 20, 128, 3), 1, 20, True),
 ]
 
 
@@ -198,7 +228,7 @@ def _run_case(case, variant):
     inp = synth.make_inputs(H, W, widths[0], widths, batch=batch, seed=seed, latent="normal",
                             latent_scale=1.5, bias="normal", shared_weights=shared)
     nl = len(widths) - 1
-    if variant in ("mfma_f32", "mfma_f16x3") and not (2 <= nl <= 4):
+    if variant in ("mfma_f32", "mfma_f16x3") and not (2 <= nl <= 4 and max(widths[1:-1]) <= 64):
         with pytest.raises(D.PicError) as e:
             gpu_decode(inp, variant=variant)
         assert e.value.status == D.PIC_E_UNSUPPORTED
@@ -259,13 +289,14 @@ def test_one_image_tile_ranges_per_xcd(variant):
     # counter of its own; 1920x1080 has 4050 tiles (not a multiple of 8) and
     # more tiles than workgroups, so the ranges are uneven and the counters
     # run.  Every pixel must be written (the output starts as NaN) and match
-    # the oracle on sampled rows, on two runs of one handle.
+    # the oracle, on two runs of one handle.
     from paper_2609_09020_amd import Decoder
     H, W = 1080, 1920
     wdt = "bf16" if variant == "mfma_bf16" else "f32"
     inp = synth.make_inputs(H, W, 7, (7, 40, 40, 3), seed=5, bias="normal", weight_dtype=wdt)
     lat, w, b = _to_dev(inp)
     dec = Decoder(H, W, inp.widths, weight_dtype=wdt, clamp=False, max_batch=1, variant=variant)
+    ref = oracle.decode_inputs(inp, out="raw")
     for run in range(2):
         out = torch.full((1, 3, H, W), float("nan"), device="cuda")
         dec.run(lat, w, b, out=out)
@@ -274,15 +305,12 @@ def test_one_image_tile_ranges_per_xcd(variant):
         print(f"PARITY xcd ranges {variant} run {run}: unwritten {int(np.count_nonzero(~np.isfinite(got)))}",
               flush=True)
         assert np.isfinite(got).all()
-        for rows in _strips(H):
-            ref = oracle.decode_inputs(inp, out="raw", rows=rows)
-            g = got[:, :, rows[0]:rows[1]]
-            if wdt == "bf16":
-                err = np.max(np.abs(g - ref) / np.maximum(1.0, np.abs(ref)))
-                print(f"PARITY xcd ranges {variant} run {run} rows{rows}: max err {err:.3e}", flush=True)
-                assert err <= BF16_TOL
-            else:
-                _check_float(g, ref, True, f"xcd ranges {variant} run {run} rows{rows}")
+        if wdt == "bf16":
+            err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
+            print(f"PARITY xcd ranges {variant} run {run}: max err {err:.3e}", flush=True)
+            assert err <= BF16_TOL
+        else:
+            _check_float(got, ref, True, f"xcd ranges {variant} run {run}")
     dec.close()
 
 
@@ -329,25 +357,6 @@ def test_run_rejects_bad_arguments_before_launch():
 
 # ------------------------------------------------------- bf16-weight family
 
-BF16_TOL = 4e-3
-
-
-def test_workload_bf16_clamped_and_raw():
-    wl = synth.WORKLOADS["uhd4k_bf16"]
-    inp = synth.workload_inputs(wl)
-    got, info = gpu_decode(inp)                       # AUTO picks the bf16 family
-    assert info["variant"] == "mfma_bf16"
-    raw, _ = gpu_decode(inp, variant="mfma_bf16", clamp=False)
-    for rows in _strips(wl.height):
-        ref = oracle.decode_inputs(inp, out="clamped", rows=rows)
-        err = np.max(np.abs(got[:, :, rows[0]:rows[1]] - ref))
-        print(f"PARITY uhd4k_bf16 mfma_bf16 clamped rows{rows}: max err {err:.3e}", flush=True)
-        assert err <= BF16_TOL
-        refr = oracle.decode_inputs(inp, out="raw", rows=rows)
-        errr = np.max(np.abs(raw[:, :, rows[0]:rows[1]] - refr) / np.maximum(1.0, np.abs(refr)))
-        print(f"PARITY uhd4k_bf16 mfma_bf16 raw rows{rows}: max err {errr:.3e}", flush=True)
-        assert errr <= BF16_TOL
-
 
 @pytest.mark.parametrize("variant", ["mfma_bf16", "mfma_f32", "valu"])
 @pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(16, 4242), ids=str)
@@ -357,7 +366,7 @@ def test_fuzz_bf16_weights(case, variant):
     inp = synth.make_inputs(H, W, widths[0], widths, batch=batch, seed=seed, latent="normal",
                             latent_scale=1.5, bias="normal", shared_weights=shared, weight_dtype="bf16")
     nl = len(widths) - 1
-    if variant != "valu" and not (2 <= nl <= 4):
+    if variant != "valu" and not (2 <= nl <= 4 and max(widths[1:-1]) <= 64):
         with pytest.raises(D.PicError) as e:
             gpu_decode(inp, variant=variant)
         assert e.value.status == D.PIC_E_UNSUPPORTED
@@ -511,7 +520,7 @@ def test_run_layers_and_fuse_reject_bad_arguments():
     f = D.pic_fuse_modulation
     p = w0.data_ptr()
     assert f(0, 4, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
-    assert f(4, 65, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
+    assert f(4, 129, 1, p, 0, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
     assert f(4, 4, 1, p, 3, p, 0, p, p, p, p, 0, p, p) == D.PIC_E_INVALID
     assert f(4, 4, 1, p, 0, p, 0, p, p, p, 0, 0, p, p) == D.PIC_E_INVALID
     torch.cuda.synchronize()
