@@ -26,14 +26,14 @@
 //   so steps over padding are skipped.  Lane group g of the first layer's B
 //   operand supplies level 4 s + g of the lane's pixel at K step s.
 //
-//   Weights are gathered once per workgroup into LDS in that operand layout
-//   (zero padded).  The first layer's operands are then held in VGPRs; the
-//   hidden layers' are read from LDS as needed (16 bytes per lane cover four
-//   K steps), which keeps VGPR use low enough for 3-5 wavefronts per SIMD;
-//   biases (accumulator layout) and the output layer's weights are read from
-//   LDS per 16-pixel group too.  The output layer (3 neurons) runs on the vector ALU: each
-//   lane forms partial sums over the hidden values it holds and two cross-lane
-//   swaps add the four lane groups.
+//   The first layer's operands are loaded once per workgroup straight into
+//   VGPRs.  The hidden matrices, the biases and the output layer's weights
+//   are copied once per workgroup into LDS, zero padded, at positions that
+//   make every operand a contiguous 16-byte read (see swz below), and read
+//   from there per 16-pixel group, which keeps VGPR use low enough for 3-5
+//   wavefronts per SIMD.  The output layer (3 neurons) runs on the vector
+//   ALU: each lane forms partial sums over the hidden values it holds and two
+//   cross-lane swaps add the four lane groups.
 //
 //   fp32 matrix and vector instructions share a SIMD's issue capacity, so the
 //   per-group vector work is kept small: fixed-offset bilinear taps, ReLU as
@@ -49,22 +49,33 @@ namespace mfma_f32 {
 
 using namespace tile;
 
+// Operand placement.  Output neuron 16 ob + 4 r + g sits on accumulator row
+// 4 g + r of block ob (lane group g, register r), and a hidden layer's K step
+// (q, r) takes inputs 16 q + 4 r + g.  In LDS each 16-neuron group is stored
+// with the two 2-bit halves of its index swapped, swz(n), for both the rows
+// (output neurons) and the columns (inputs) of a matrix and for the bias and
+// output-layer vectors.  A lane's four K steps of a quad are then one
+// contiguous 16-byte read: row swz(16 ob + rn(i)) = 16 ob + i holds, at
+// columns 16 q + 4 g .. + 3, inputs 16 q + 4 r + g for r = 0 .. 3; its
+// accumulator-layout bias is the 16 bytes at 16 ob + 4 g, and so are its
+// output-layer weights.  The staging needs no index arithmetic either: a
+// wavefront copies whole matrix rows, one column per lane, so the row part
+// of every address is uniform and the column part is the lane's own.
+__host__ __device__ constexpr int swz(int n) { return (n & ~15) | ((n & 3) << 2) | ((n >> 2) & 3); }
+
 template <int NB, int NH, int LS, int KSH>
 struct Layout {
-    static constexpr int W1A = 0;                                   // [NB][LS][64]
+    static constexpr int N = 16 * NB;                               // padded hidden width
     static constexpr int KSH4 = (KSH + 3) / 4;                      // quads of hidden K steps
-    static constexpr int WHA = W1A + NB * LS * 64;                  // [NH][NB][KSH4][64][4 steps]
-    static constexpr int B1 = WHA + NH * NB * KSH4 * 256;           // [NB][64][4]
-    static constexpr int BH = B1 + NB * 64 * 4;                     // [NH][NB][64][4]
-    static constexpr int W3 = BH + NH * NB * 64 * 4;                // [NB][4 r][4 g][4 c]
-    static constexpr int LAT = W3 + NB * 4 * 4 * 4;                 // latent boxes
+    // row pitch of a staged hidden matrix: a multiple of 4 floats (16-byte
+    // reads) with pitch / 4 odd, so the 16 rows one lane group reads fall in
+    // distinct 16-byte bank groups
+    static constexpr int PITCH = N + 4;
+    static constexpr int WH = 0;                                    // [NH][N rows][PITCH]
+    static constexpr int BIAS = WH + NH * N * PITCH;                // [NH + 1][N]
+    static constexpr int W3 = BIAS + (NH + 1) * N;                  // [3][N]
+    static constexpr int LAT = W3 + 3 * N;                          // latent boxes
     static constexpr int SIZE = LAT + box_offset(4 * LS);
-    // the parameters as the caller lays them out are first staged in the
-    // regions their operand layouts then replace (each is at least as large)
-    static constexpr int N = 16 * NB;
-    static_assert(N * 4 * LS <= NB * LS * 64, "layer 1 fits its region");
-    static_assert(N * N <= NB * KSH4 * 256 || KSH < 4 * NB, "hidden layers fit their regions");
-    static_assert(3 * N <= NB * 64, "output layer fits its region");
 };
 
 // Neuron on row `row` of an output block; the map is its own inverse.
@@ -78,11 +89,13 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
     using LY = Layout<NB, NH, LS, KSH>;
+    constexpr int N = LY::N, PITCH = LY::PITCH;
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
 
     warm_kernel_args<sizeof(DecodeParams)>();
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, col = lane & 15;
     // images interleave over the grid, so that every image's workgroups are
     // spread over the dispatch order (older workgroups on a CU run ahead)
@@ -96,15 +109,13 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
 
     float boxv[box_regs<4 * LS>()];
+    float w1[NB][LS];
 
-    // ---- stage this image's parameters into LDS in operand layouts: first
-    // as the caller lays them out, with contiguous loads all in flight at
-    // once, then permuted through registers
+    // ---- parameters.  Every load is issued before the first is waited for:
+    // the first layer's operands straight into registers, the hidden
+    // matrices' rows, biases and output weights into registers, then the
+    // first tile's latent boxes; after that everything is stored to LDS.
     {
-        // every layer's pointers and widths first (one batch of scalar
-        // loads), then the loads themselves: raw copies whose entries past
-        // the layer's size hold anything (the permutation reads only valid
-        // ones), so no load is waited for before the latents' go out
         LayerParams lp[NH + 2];
         int wd[NH + 3];
 #pragma unroll
@@ -114,103 +125,90 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         for (int l = 0; l < NH + 3; ++l)
             wd[l] = p.widths[l];
         const int N1 = wd[1], NL = wd[NH + 1];
-        constexpr int KSH4 = LY::KSH4;
-        // raw copies: layer 1 in W1A, hidden layer h in its WHA block (or, when
-        // the last K steps are skipped and the block is smaller, in the box
-        // area), the output layer in W3, biases in B1 / BH
-        constexpr int RAW_H = LY::N * LY::N <= NB * KSH4 * 256 ? 0 : 1;
-        static_assert(!RAW_H || NH * LY::N * LY::N <= box_offset(4 * LS), "hidden layers fit the box area");
-        auto raw_h = [&](int h) { return RAW_H ? LY::LAT + h * LY::N * LY::N : LY::WHA + h * NB * KSH4 * 256; };
-        Part<LY::N, float> rb[NH + 1];
-#pragma unroll
-        for (int h = 0; h <= NH; ++h) {
-            const int fout = wd[1 + h];
-            rb[h] = load_part<LY::N, float>([&](int s) { return lp[h].bias_clamped(s, fout); });
-        }
-        Part<LY::N * 4 * LS, float> r1;
-        Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
-        Part<3 * LY::N, float> r3;
-        // one straight run of loads per weight type (uniform branch)
-        auto load_weights = [&](auto bf16) {
+        constexpr int RW = N / 4;                  // matrix rows per wavefront
+        float hrow[NH > 0 ? NH : 1][RW];
+        float bv, w3v;
+        // Every load reads an in-range entry (indices clamped into the
+        // arrays) and none sits behind a branch or feeds a select before the
+        // last load is issued: entries outside a layer's shape are zeroed
+        // when stored, after the latent loads have gone out, so no wait is
+        // placed between the loads.  A row's address is uniform (scalar
+        // registers) plus the lane's byte offset, the same for every row.
+        const int lw = min(wave, NH), l3 = min(wave, 2);    // bias layer / output row of this wavefront
+        auto load_all = [&](auto bf16) {
             constexpr bool BF = decltype(bf16)::value;
-            r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return lp[0].template weight_clamped<BF>(s, N1 * L); });
+            using T = typename std::conditional<BF, uint16_t, float>::type;
+            auto widen = [](T v) {
+                if constexpr (BF)
+                    return __uint_as_float((uint32_t)v << 16);
+                else
+                    return v;
+            };
+            auto at = [](const T *row, unsigned byte_off) {
+                return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(row) + byte_off);
+            };
+            // layer 1, A operand: lane (g, i) holds W1[16 ob + rn(i)][4 s + g]
+            const T *w1p = static_cast<const T *>(lp[0].w);
+            const int r1 = row_neuron(col);
+#pragma unroll
+            for (int ob = 0; ob < NB; ++ob)
+#pragma unroll
+                for (int s = 0; s < LS; ++s)
+                    w1[ob][s] = widen(w1p[min(16 * ob + r1, N1 - 1) * L + min(4 * s + g, L - 1)]);
+            // hidden layer h: wavefront w copies rows w, w + 4, ..., lane c column c
 #pragma unroll
             for (int h = 0; h < NH; ++h) {
-                const int n = wd[1 + h] * wd[2 + h];
-                rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return lp[1 + h].template weight_clamped<BF>(s, n); });
+                const int fin = wd[1 + h], fout = wd[2 + h];
+                const T *wp = static_cast<const T *>(lp[1 + h].w);
+                const unsigned cb = (unsigned)min(lane, fin - 1) * sizeof(T);
+#pragma unroll
+                for (int t = 0; t < RW; ++t)
+                    hrow[h][t] = widen(at(wp + (int64_t)min(wave + 4 * t, fout - 1) * fin, cb));
             }
-            r3 = load_part<3 * LY::N, float>([&](int s) { return lp[NH + 1].template weight_clamped<BF>(s, 3 * NL); });
+            // the bias of layer min(w, NH); row min(w, 2) of the output layer
+            // (kernel-argument arrays indexed by the uniform wave number)
+            const float *bsrc = p.bl[lw] + (int64_t)b * p.bls[lw];
+            bv = bsrc[min(lane, p.widths[1 + lw] - 1)];
+            const T *w3p = static_cast<const T *>(lp[NH + 1].w) + l3 * NL;
+            w3v = widen(at(w3p, (unsigned)min(lane, NL - 1) * sizeof(T)));
         };
         if (lp[0].bf16)
-            load_weights(std::true_type{});
+            load_all(std::true_type{});
         else
-            load_weights(std::false_type{});
+            load_all(std::false_type{});
         // the first tile's latent loads go out behind the parameters: loads
-        // complete in order, so the permutation below need not wait for them
+        // complete in order, so the stores below need not wait for them
         if (blk < tiles)
             load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
-        store_part(lds + LY::W1A, r1);
+        // zero what lies outside each layer's shape
+        const int r1 = row_neuron(col);
 #pragma unroll
-        for (int h = 0; h < NH; ++h)
-            store_part(lds + raw_h(h), rh[h]);
-        store_part(lds + LY::W3, r3);
+        for (int ob = 0; ob < NB; ++ob)
 #pragma unroll
-        for (int h = 0; h <= NH; ++h)
-            store_part(lds + LY::B1 + h * NB * 256, rb[h]);
-        __syncthreads();
-
-        const auto w1a = load_part<NB * LS * 64, float>([&](int s) {          // layer 1, A layout
-            const int ln = s & 63, step = (s >> 6) % LS, ob = (s >> 6) / LS;
-            const int out = 16 * ob + row_neuron(ln & 15), in = 4 * step + (ln >> 4);
-            return (out < N1 && in < L) ? lds[LY::W1A + out * L + in] : 0.0f;
-        });
-        Part<NB * KSH4 * 256, float> wha[NH > 0 ? NH : 1];
+            for (int s = 0; s < LS; ++s)
+                w1[ob][s] = (16 * ob + r1 < N1 && 4 * s + g < L) ? w1[ob][s] : 0.0f;
+        if (lane < N) {
+            // row wave + 4 t goes to swz(wave + 4 t) = 16 (t / 4) + 4 wave + t % 4
+            // (wave < 4): a per-lane base plus a constant per row
+            const int sc = swz(lane);
+            float *wrow = lds + LY::WH + 4 * wave * PITCH + sc;
 #pragma unroll
-        for (int h = 0; h < NH; ++h) {                                         // hidden layers, A layout
-            const int fin = p.widths[1 + h], fout = p.widths[2 + h];
-            wha[h] = load_part<NB * KSH4 * 256, float>([&](int s) {
-                const int j = s & 3, ln = (s >> 2) & 63, q = (s >> 8) % KSH4, ob = (s >> 8) / KSH4;
-                const int ks = 4 * q + j;
-                const int out = 16 * ob + row_neuron(ln & 15);
-                const int in = 16 * (ks >> 2) + 4 * (ks & 3) + (ln >> 4);
-                return (ks < KSH && out < fout && in < fin) ? lds[raw_h(h) + out * fin + in] : 0.0f;
-            });
+            for (int h = 0; h < NH; ++h) {
+                const bool cin = lane < wd[1 + h];
+                const int fout = wd[2 + h];
+#pragma unroll
+                for (int t = 0; t < RW; ++t)
+                    wrow[(h * N + 16 * (t >> 2) + (t & 3)) * PITCH] = (cin && wave + 4 * t < fout) ? hrow[h][t] : 0.0f;
+            }
+            if (wave <= NH)
+                lds[LY::BIAS + wave * N + sc] = lane < p.widths[1 + lw] ? bv : 0.0f;
+            if (wave < 3)
+                lds[LY::W3 + wave * N + sc] = lane < NL ? w3v : 0.0f;
         }
-        Part<NB * 256, float> bias[NH + 1];
-#pragma unroll
-        for (int h = 0; h <= NH; ++h) {                                        // biases, accumulator layout
-            const int fout = p.widths[1 + h];
-            bias[h] = load_part<NB * 256, float>([&](int s) {
-                const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
-                const int n = 16 * ob + 4 * r + (ln >> 4);
-                return n < fout ? lds[LY::B1 + h * NB * 256 + n] : 0.0f;
-            });
-        }
-        const auto w3 = load_part<NB * 64, float>([&](int s) {                // output layer [ob][r][g][c]
-            const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
-            const int n = 16 * ob + 4 * r + gg;
-            return (c < 3 && n < NL) ? lds[LY::W3 + c * NL + n] : 0.0f;
-        });
-        __syncthreads();                   // every raw value is read
-        store_part(lds + LY::W1A, w1a);
-#pragma unroll
-        for (int h = 0; h < NH; ++h)
-            store_part(lds + LY::WHA + h * NB * KSH4 * 256, wha[h]);
-#pragma unroll
-        for (int h = 0; h <= NH; ++h)
-            store_part(lds + LY::B1 + h * NB * 256, bias[h]);
-        store_part(lds + LY::W3, w3);
     }
     if (blk < tiles)
         store_boxes<4 * LS>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
-
-    float w1[NB][LS];
-#pragma unroll
-    for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-        for (int s = 0; s < LS; ++s)
-            w1[ob][s] = lds[LY::W1A + (ob * LS + s) * 64 + lane];
 
     // ---- the level each lane samples for K step s of the first layer.  Lanes
     // whose level 4 s + g does not exist sample level 0 instead: their
@@ -229,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
     constexpr int KS1 = KSH;   // live registers of a hidden activation
-    constexpr int W3CH = 6;   // (larger chunks raise the VGPR count of the wider shapes)
+    constexpr int W3NB = 2;   // (larger chunks raise the VGPR count of the wider shapes)
 
     // Tiles: the workgroup's first is tile blk; the others come from its
     // schedule's counter (tile ts.base + ticket, while below ts.end), so that
@@ -285,7 +283,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                 f32x4 d[NB];
 #pragma unroll
                 for (int ob = 0; ob < NB; ++ob)
-                    d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + (ob * 64 + lane) * 4]);
+                    d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + 16 * ob + 4 * g]);
 #pragma unroll
                 for (int s = 0; s < LS; ++s) {
                     const float u = lane_level_sample(lds, lv[s], roff[s], rly[s], cg);
@@ -303,7 +301,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
                     f32x4 e[NB];
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
-                        e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BH + ((h * NB + ob) * 64 + lane) * 4]);
+                        e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + (1 + h) * N + 16 * ob + 4 * g]);
                     // A operands of K steps 4q .. 4q+3 come from LDS, one 16-byte
                     // read per output block; step 4q + j pairs with register j
                     // of input block q.
@@ -313,7 +311,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 #pragma unroll
                         for (int ob = 0; ob < NB; ++ob)
                             wq[ob] = *reinterpret_cast<const f32x4 *>(
-                                &lds[LY::WHA + ((h * NB + ob) * LY::KSH4 + q) * 256 + lane * 4]);
+                                &lds[LY::WH + (h * N + 16 * ob + col) * PITCH + 16 * q + 4 * g]);
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
                             if (4 * q + j < KSH) {
@@ -330,23 +328,28 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 
                 // output layer on the vector ALU: partial sums over this lane's
                 // live hidden values, then a sum over the four lane groups
-                // (weights are read W3CH at a time, all before their first use,
-                // so one LDS round trip covers each chunk)
+                // (weights of W3NB blocks are read at a time, all before their
+                // first use, so one LDS round trip covers each chunk)
                 float o0 = ob0, o1 = ob1, o2 = ob2;
 #pragma unroll
-                for (int k0 = 0; k0 < KS1; k0 += W3CH) {
-                    f32x4 w3[W3CH];
+                for (int nb0 = 0; nb0 < NB; nb0 += W3NB) {
+                    f32x4 w3[W3NB][3];
 #pragma unroll
-                    for (int j = 0; j < W3CH; ++j)
-                        if (k0 + j < KS1)
-                            w3[j] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((k0 + j) * 4 + g) * 4]);
+                    for (int j = 0; j < W3NB; ++j)
+                        if (nb0 + j < NB)
 #pragma unroll
-                    for (int j = 0; j < W3CH; ++j) {
-                        if (k0 + j < KS1) {
-                            const float hv = d[(k0 + j) >> 2][(k0 + j) & 3];
-                            o0 = __builtin_fmaf(w3[j][0], hv, o0);
-                            o1 = __builtin_fmaf(w3[j][1], hv, o1);
-                            o2 = __builtin_fmaf(w3[j][2], hv, o2);
+                            for (int c = 0; c < 3; ++c)
+                                w3[j][c] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + c * N + 16 * (nb0 + j) + 4 * g]);
+#pragma unroll
+                    for (int j = 0; j < W3NB; ++j) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            if (nb0 + j < NB && 4 * (nb0 + j) + r < KS1) {
+                                const float hv = d[nb0 + j][r];
+                                o0 = __builtin_fmaf(w3[j][0][r], hv, o0);
+                                o1 = __builtin_fmaf(w3[j][1][r], hv, o1);
+                                o2 = __builtin_fmaf(w3[j][2][r], hv, o2);
+                            }
                         }
                     }
                 }
@@ -369,7 +372,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 
 int hidden_blocks(int nl, const int32_t *widths);
 
-// Hidden K steps the shape needs: ceil(width / 4) of the widest hidden input.
+// Hidden K steps the shape needs: ceil(width / 4) of the widest hidden layer.
+// Every hidden activation is the input of a later layer (the next hidden
+// layer or the output layer), and the K-step count also bounds the ReLU and
+// the output layer's sums, so the last hidden width counts as well.
 int hidden_ksteps(int nl, const int32_t *widths);
 
 template <int NB, int NH, int LS, int KSH>
