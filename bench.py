@@ -12,9 +12,19 @@ Prints ONE JSON line: decoded Mpixel/s (value), FPS, ms per step, the
 roofline of the dominant kernel and the CPU oracle's throughput on a bounded
 sample of the same workload (rank 0, N = 1 only).
 
+The same line carries `per_config`: every other workload of the benchmark
+suite (64x64; 768x512 x64; 2048x1536 x1 and x16; 3840x2160 with fp32 and
+with bf16 weights; the paper's 4-layer net at 768x512), each timed after the
+headline's timed region with HIP events over back-to-back launches, with its
+roofline fraction; and `paper_context`: the paper's own decoding speed with
+the hardware it was measured on (context, not the target).
+
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload kodak768]
-                  [--variant auto|valu|mfma_f32|mfma_bf16] [--out-dtype f32|u8]
-                  [--no-cpu-baseline] [--copy-calib]
+                  [--variant auto|valu|mfma_f32|mfma_bf16|mfma_f16x3]
+                  [--out-dtype f32|u8] [--no-cpu-baseline] [--no-per-config]
+                  [--copy-calib]
+  python bench.py --peaks        peak issue rates of the matrix and vector
+                                 units and the device-copy bandwidth
 """
 from __future__ import annotations
 
@@ -34,6 +44,7 @@ PEAK_FP32_TFLOPS = 157.3        # fp32 vector (packed) and fp32 matrix
 PEAK_BF16_TFLOPS = 2500.0       # dense bf16 matrix
 PEAK_FP16_TFLOPS = 2500.0       # dense fp16 matrix
 PEAK_HBM_GBS = 8000.0
+CLOCK_HZ = 2.4e9                # peak engine clock
 
 
 def flops_per_pixel(widths):
@@ -143,6 +154,157 @@ def time_calls(run, K, W, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / K, time.perf_counter() - t0
+
+
+def variant_peak(variant):
+    """(bound, peak, unit) of the dominant instructions of a kernel family."""
+    if variant == "mfma_bf16":
+        return "mfma", PEAK_BF16_TFLOPS, "TFLOP/s"
+    if variant == "mfma_f32":
+        return "mfma", PEAK_FP32_TFLOPS, "TFLOP/s"
+    if variant == "mfma_f16x3":
+        # fp32 arithmetic carried out on the fp16 matrix cores: against the
+        # peak of the instructions it runs on (its fp32-equivalent rate beside)
+        return "mfma", PEAK_FP16_TFLOPS, "TFLOP/s"
+    return "alu", PEAK_FP32_TFLOPS, "TFLOP/s"
+
+
+# The paper's own decoding speed (Table 1; Sec. 4.1): the whole decoder,
+# entropy decoding included, per Kodak image, serially, on its GPU.
+PAPER_CONTEXT = {
+    "fps": 2392, "ms_per_image": 0.418, "mpixel_s": round(768 * 512 / 0.418e-3 / 1e6, 1),
+    "hardware": "1x NVIDIA RTX 4090D", "precision": "TF32 tensor cores",
+    "workload": "Kodak (24 images of 768x512), whole decoder (entropy decoding, latent decoding, "
+                "synthesis), L = 8 levels, g_s 4 layers of width 16, images decoded one at a time",
+    "source": "Table 1 (decode time), Sec. 4.1",
+    "note": "context only: another machine and the whole decoder; `bench.py --full` times the "
+            "whole decoder here",
+}
+
+# Workloads of the benchmark suite timed beside the headline one (per_config).
+PER_CONFIG = ["pic64", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k", "uhd4k_bf16", "kodak768_paper"]
+
+
+def time_workload(name, variant="auto", out_dtype="f32", target_s=0.3):
+    """Kernel time of one workload: HIP events on the launch stream around
+    back-to-back pic_decode_run calls (about target_s seconds of them)."""
+    import ctypes
+    import numpy as np
+    import torch
+    from paper_2609_09020_amd import synth
+    from paper_2609_09020_amd import decoder as D
+    wl = synth.WORKLOADS[name]
+    inp = synth.workload_inputs(wl)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
+    w = torch.from_numpy(inp.weights_bf16.view(np.int16) if inp.weights_bf16 is not None else inp.weights).to(dev)
+    b = torch.from_numpy(inp.biases).to(dev)
+    dec = D.Decoder(wl.height, wl.width, wl.widths, weight_dtype=wl.weight_dtype, out_dtype=out_dtype,
+                    max_batch=wl.batch, variant=variant)
+    out = dec.alloc_out(wl.batch, dev)
+    lib = D.load_library()
+    lat_arr = (ctypes.c_void_p * len(lat))(*[t.data_ptr() for t in lat])
+    run_args = (ctypes.c_void_p(dec.handle), ctypes.c_int32(wl.batch), lat_arr, ctypes.c_void_p(w.data_ptr()),
+                ctypes.c_int64(dec.nw), ctypes.c_void_p(b.data_ptr()), ctypes.c_int64(dec.nb),
+                ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+
+    def launches(n):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            st = lib.pic_decode_run(*run_args)
+            if st != D.PIC_OK:
+                raise D.PicError(st, "pic_decode_run")
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    launches(10)                                   # warm-up
+    est = launches(5)
+    n = int(min(4000, max(20, target_s * 1e3 / max(est, 1e-4))))
+    ms = launches(n)
+    info = dec.info()
+    dec.close()
+    px = wl.batch * wl.height * wl.width
+    fpp = flops_per_pixel(wl.widths)
+    bound, peak, unit = variant_peak(info["variant"])
+    achieved = px * fpp / (ms * 1e-3) / 1e12
+    return {"workload": f"{wl.name}: {wl.note}", "widths": list(wl.widths), "batch": wl.batch,
+            "weights": wl.weight_dtype, "variant": info["variant"], "kernel": info["kernel_name"],
+            "launches": n, "kernel_avg_ms": round(ms, 5), "mpixel_s": round(px / ms / 1e3, 1),
+            "fps": round(wl.batch / ms * 1e3, 1),
+            "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                         "frac": round(achieved / peak, 4),
+                         "fp32_equivalent_frac": round(achieved / PEAK_FP32_TFLOPS, 4),
+                         "flop_per_pixel": fpp}}
+
+
+def peaks(args):
+    """Peak issue rates on this GPU (SURVEY-style microbenchmarks, used to
+    ground the design): fp32 / bf16 / fp16 matrix instructions and fp32 vector
+    FMAs, each with independent accumulators, the fp32 and bf16 matrix
+    instructions interleaved with vector FMAs in the same wavefronts, and a
+    device-to-device copy.  One JSON line per measurement."""
+    import ctypes
+    import torch
+    from paper_2609_09020_amd import build as B
+    lib = ctypes.CDLL(B.PEAKS_LIB)
+    lib.pic_peaks_launch.restype = ctypes.c_int
+    lib.pic_peaks_launch.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    props = torch.cuda.get_device_properties(dev)
+    cus = props.multi_processor_count
+    # (name, matrix FLOP per iteration per wavefront, vector FLOP per iteration per wavefront)
+    kinds = [("fp32 matrix v_mfma_f32_16x16x4_f32", 8 * 2048, 0),
+             ("bf16 matrix v_mfma_f32_16x16x32_bf16", 8 * 16384, 0),
+             ("fp16 matrix v_mfma_f32_16x16x32_f16", 8 * 16384, 0),
+             ("fp32 vector v_fma_f32 (not packed)", 0, 32 * 128),
+             ("fp32 matrix + fp32 vector, interleaved", 8 * 2048, 32 * 128),
+             ("bf16 matrix + fp32 vector, interleaved", 8 * 16384, 32 * 128)]
+    alone = {}
+    for waves_per_simd in (1, 2, 4):
+        blocks = cus * waves_per_simd                  # 4 wavefronts per workgroup: one per SIMD
+        out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+        for kind, (what, mf, vf) in enumerate(kinds):
+            iters = 20000 if kind != 3 else 40000
+
+            def launch():
+                st = lib.pic_peaks_launch(kind, blocks, iters, ctypes.c_void_p(out.data_ptr()),
+                                          ctypes.c_void_p(stream.cuda_stream))
+                if st:
+                    raise RuntimeError(f"pic_peaks_launch({kind}) failed: {st}")
+            launch()
+            torch.cuda.synchronize()
+            ms, _ = time_calls(launch, 5, 1, stream)
+            waves = blocks * 4
+            mt = mf * iters * waves / (ms * 1e-3) / 1e12
+            vt = vf * iters * waves / (ms * 1e-3) / 1e12
+            # cycles at the published 2.4 GHz engine clock
+            cyc = ms * 1e-3 * CLOCK_HZ / (waves_per_simd * iters)
+            rec = {"peaks": what, "waves_per_simd": waves_per_simd, "ms": round(ms, 4),
+                   "matrix_tflops": round(mt, 1), "vector_tflops": round(vt, 1),
+                   "cycles_per_iteration_per_simd": round(cyc * waves_per_simd, 1),
+                   "cycles_per_iteration_per_wave": round(cyc, 1)}
+            # per-iteration cycles per SIMD: the mixed kernels against the sum
+            # of their parts (0: the parts serialise, 1: the shorter is hidden)
+            if kind < 4:
+                alone[(kind, waves_per_simd)] = cyc * waves_per_simd
+            else:
+                a = alone[(0 if kind == 4 else 1, waves_per_simd)]
+                v = alone[(3, waves_per_simd)]
+                both = cyc * waves_per_simd
+                rec["sum_of_parts_cycles_per_simd"] = round(a + v, 1)
+                rec["overlap_frac"] = round((a + v - both) / min(a, v), 3)
+            print(json.dumps(rec), flush=True)
+    n = 1 << 30
+    src = torch.full((n,), 7, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    ms, _ = time_calls(lambda: dst.copy_(src), 20, 3, stream)
+    print(json.dumps({"peaks": "device copy (torch copy_ of 1 GiB)", "ms": round(ms, 4),
+                      "read_plus_write_gbs": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def width_sweep(args):
@@ -393,6 +555,10 @@ def main():
     ap.add_argument("--variant", default="auto")
     ap.add_argument("--out-dtype", default="f32", choices=["f32", "u8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="leave out the other workloads' timings (per_config)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="instead of the benchmark line, measure peak issue rates and copy bandwidth")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain device copy of known size (counter calibration)")
     ap.add_argument("--width-sweep", action="store_true",
@@ -422,6 +588,9 @@ def main():
 
     if args.width_sweep:
         width_sweep(args)
+        return
+    if args.peaks:
+        peaks(args)
         return
     for flag, stages in ((args.full, ("huff", "zpr", "synth")), (args.pipeline, ("zpr", "synth")),
                          (args.huff, ("huff",)), (args.zpr, ("zpr",))):
@@ -503,16 +672,7 @@ def main():
     fpp = flops_per_pixel(wl.widths)
     flop = px * fpp
     kernel = info["kernel_name"]
-    if info["variant"] == "mfma_bf16":
-        bound, peak, unit = "mfma", PEAK_BF16_TFLOPS, "TFLOP/s"
-    elif info["variant"] == "mfma_f32":
-        bound, peak, unit = "mfma", PEAK_FP32_TFLOPS, "TFLOP/s"
-    elif info["variant"] == "mfma_f16x3":
-        # fp32 arithmetic carried out on the fp16 matrix cores: against the
-        # peak of the instructions it runs on (its fp32-equivalent rate beside)
-        bound, peak, unit = "mfma", PEAK_FP16_TFLOPS, "TFLOP/s"
-    else:
-        bound, peak, unit = "alu", PEAK_FP32_TFLOPS, "TFLOP/s"
+    bound, peak, unit = variant_peak(info["variant"])
     achieved = flop / (kern_avg_ms * 1e-3) / 1e12
     traffic = load_traffic(kernel, args.workload, args.out_dtype)
     res = {
@@ -535,9 +695,15 @@ def main():
                      "hbm_frac_at_compulsory_bytes": round(
                          bytes_per_call(wl, args.out_dtype) / (kern_avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
+    dec.close()
+    del lat, w, b, out
+    res["paper_context"] = PAPER_CONTEXT
+    if not args.no_per_config:
+        res["per_config"] = {name: time_workload(name, out_dtype=args.out_dtype)
+                             for name in PER_CONFIG if name != args.workload}
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, inp)
-    dec.close()
     print(json.dumps(res), flush=True)
 
 

@@ -1,7 +1,9 @@
-"""Build the HIP library libpic_decode.so for gfx950 (in-tree).
+"""Build the HIP libraries for gfx950 (in-tree).
 
 Every translation unit under csrc/ is compiled by hipcc in parallel into
-_build/, then linked into paper_2609_09020_amd/libpic_decode.so.  Flags:
+_build/, then linked into paper_2609_09020_amd/libpic_decode.so (the
+decoder).  peaks/k_peaks.hip becomes libpic_peaks.so: the peak-rate
+microbenchmarks `bench.py --peaks` runs, not part of the decoder.  Flags:
   -ffp-contract=off          multiplies and adds round exactly as written;
                               fused operations are spelled out as fmaf
   -packed-fp32-ops disabled  no packed fp32 VALU instructions are emitted
@@ -21,6 +23,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpic_decode.so")
+PEAKS_SRC = os.path.join(PKG, "peaks", "k_peaks.hip")
+PEAKS_LIB = os.path.join(PKG, "libpic_peaks.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -48,19 +52,25 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sources()
-    with cf.ThreadPoolExecutor(max_workers=min(jobs, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB + f".tmp{os.getpid()}"
+def _link(objs, lib, verbose):
+    tmp = lib + f".tmp{os.getpid()}"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False, jobs: int = 8) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    # the wide reference-family instances take longest to compile: start them first
+    srcs = sorted(sources() + [PEAKS_SRC], key=lambda s: 0 if "_w128" in s or "_w96" in s else 1)
+    with cf.ThreadPoolExecutor(max_workers=min(jobs, len(srcs))) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose), srcs)))
+    _link([objs[s] for s in sources()], LIB, verbose)
+    _link([objs[PEAKS_SRC]], PEAKS_LIB, verbose)
     return LIB
 
 
