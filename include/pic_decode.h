@@ -92,7 +92,8 @@ enum {
     PIC_MAX_LEVELS = 12,    /* L                                                  */
     PIC_MAX_LAYERS = 8,     /* linear layers                                      */
     PIC_MAX_WIDTH = 128,    /* hidden width                                       */
-    PIC_MAX_BATCH = 65535   /* images per call                                    */
+    PIC_MAX_BATCH = 65535,  /* images per call                                    */
+    PIC_NOALLOC_MAX_BATCH = 4096  /* images per pic_decode_run_noalloc call       */
 };
 
 /* desc.flags */
@@ -170,6 +171,33 @@ PIC_API pic_status pic_decode_run(pic_decoder *dec, int32_t batch,
                                   const void *weights, int64_t weights_img_stride,
                                   const float *biases, int64_t biases_img_stride,
                                   void *out, void *stream);
+
+/*
+ * pic_decode_run_noalloc -- pic_decode_run without a handle, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  It validates `desc` (as
+ * pic_decode_create does) and enqueues the same kernels pic_decode_run would,
+ * and it calls no hipMalloc, hipFree or other allocating routine.
+ *   desc       : read only, not retained; desc->max_batch bounds `batch`.
+ *   other arguments, layouts and ownership: as pic_decode_run.
+ * The matrix-core kernels' tile counters live in the library's own device
+ * array (16 KiB: PIC_NOALLOC_MAX_BATCH 4-byte counters, held by each GPU the
+ * library runs on until the process ends).  Each call first enqueues a small
+ * kernel that clears the counters it uses, then the decode, on `stream`.
+ * Every call on one GPU shares that array: calls that overlap on one GPU
+ * (other streams without synchronisation, or other threads) race on it and
+ * must not be made.  The first call on a device, with that device current,
+ * looks up the array's device address and the device's properties.
+ * Returns as pic_decode_run, plus PIC_E_UNSUPPORTED for batch above
+ * PIC_NOALLOC_MAX_BATCH (nothing is enqueued) and the statuses of
+ * pic_decode_create for the descriptor (PIC_E_INVALID, PIC_E_UNSUPPORTED,
+ * PIC_E_NODEVICE); PIC_E_HIP if the array's address cannot be found.
+ */
+PIC_API pic_status pic_decode_run_noalloc(const pic_decode_desc *desc, int32_t batch,
+                                          const float *const *latents,
+                                          const void *weights, int64_t weights_img_stride,
+                                          const float *biases, int64_t biases_img_stride,
+                                          void *out, void *stream);
 
 /*
  * pic_decode_run_layers -- pic_decode_run with one parameter pointer and one

@@ -2,6 +2,7 @@
 // launch on the caller's stream.  The kernels live in k_*.hip.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <new>
 #include <stdio.h>
 #include <string.h>
@@ -21,6 +22,13 @@ struct pic_decoder {
     int32_t *d_ctr;             // [2][tile_counters(max_batch)] tile counters, used by alternate runs
     uint32_t runs;              // matrix-core runs launched so far
 };
+
+// Tile counters of pic_decode_run_noalloc: one slot of tile_counters(batch)
+// per device (each GPU the library runs on holds its own copy of the array
+// until the process ends).  Host code never passes this name to a kernel or a
+// copy: it is a host-side stand-in; the device address comes from
+// hipGetSymbolAddress, once per device (noalloc_state below).
+static __device__ __align__(256) int32_t scratch[PIC_NOALLOC_MAX_BATCH];
 
 namespace {
 
@@ -56,6 +64,77 @@ pic_status validate_desc(const pic_decode_desc *d)
     return PIC_OK;
 }
 
+// The kernel family for a valid descriptor (AUTO resolved), or
+// PIC_E_UNSUPPORTED.
+pic_status resolve_variant(const pic_decode_desc *desc, int32_t *out)
+{
+    const int L = desc->num_levels, nl = desc->num_layers;
+    int32_t variant = desc->variant;
+    if (variant == PIC_VARIANT_AUTO) {
+        // Matrix cores where the family covers the shape, else the reference family.
+        if (desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths))
+            variant = PIC_VARIANT_MFMA_BF16;
+        else if (desc->weight_dtype == PIC_F32 && pic::mfma_f32_supports(L, nl, desc->widths))
+            variant = PIC_VARIANT_MFMA_F32;
+        else
+            variant = PIC_VARIANT_VALU;
+    }
+    bool ok = false;
+    switch (variant) {
+    case PIC_VARIANT_VALU: ok = pic::valu_supports(L, nl, desc->widths); break;
+    case PIC_VARIANT_MFMA_F32: ok = pic::mfma_f32_supports(L, nl, desc->widths); break;
+    case PIC_VARIANT_MFMA_BF16:
+        ok = desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths);
+        break;
+    case PIC_VARIANT_MFMA_F16X3:
+        ok = desc->weight_dtype == PIC_F32 && pic::mfma_f16x3_supports(L, nl, desc->widths);
+        break;
+    }
+    if (!ok)
+        return PIC_E_UNSUPPORTED;
+    *out = variant;
+    return PIC_OK;
+}
+
+// Compute units of device dev if it is a gfx950 (else PIC_E_NODEVICE).
+pic_status gfx950_cus(int dev, int *num_cus)
+{
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return PIC_E_NODEVICE;
+    }
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return PIC_E_NODEVICE;
+    *num_cus = prop.multiProcessorCount;
+    return PIC_OK;
+}
+
+// The current device, if there is one.
+pic_status current_device(int *dev)
+{
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1 || hipGetDevice(dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return PIC_E_NODEVICE;
+    }
+    return PIC_OK;
+}
+
+// A handle's host fields for a validated descriptor.
+void init_handle(pic_decoder *d, const pic_decode_desc *desc, int32_t variant, int dev, int num_cus)
+{
+    memset(d, 0, sizeof *d);
+    d->desc = *desc;
+    d->variant = variant;
+    d->device = dev;
+    d->num_cus = num_cus;
+    for (int l = 0; l < desc->num_layers; ++l) {
+        d->weights_per_image += (int64_t)desc->widths[l] * desc->widths[l + 1];
+        d->biases_per_image += desc->widths[l + 1];
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -81,58 +160,21 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
     pic_status st = validate_desc(desc);
     if (st != PIC_OK)
         return st;
-
-    const int L = desc->num_levels, nl = desc->num_layers;
-    int32_t variant = desc->variant;
-    if (variant == PIC_VARIANT_AUTO) {
-        // Matrix cores where the family covers the shape, else the reference family.
-        if (desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths))
-            variant = PIC_VARIANT_MFMA_BF16;
-        else if (desc->weight_dtype == PIC_F32 && pic::mfma_f32_supports(L, nl, desc->widths))
-            variant = PIC_VARIANT_MFMA_F32;
-        else
-            variant = PIC_VARIANT_VALU;
-    }
-    bool ok = false;
-    switch (variant) {
-    case PIC_VARIANT_VALU: ok = pic::valu_supports(L, nl, desc->widths); break;
-    case PIC_VARIANT_MFMA_F32: ok = pic::mfma_f32_supports(L, nl, desc->widths); break;
-    case PIC_VARIANT_MFMA_BF16:
-        ok = desc->weight_dtype == PIC_BF16 && pic::mfma_bf16_supports(L, nl, desc->widths);
-        break;
-    case PIC_VARIANT_MFMA_F16X3:
-        ok = desc->weight_dtype == PIC_F32 && pic::mfma_f16x3_supports(L, nl, desc->widths);
-        break;
-    }
-    if (!ok)
-        return PIC_E_UNSUPPORTED;
-
-    int ndev = 0;
-    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
-        (void)hipGetLastError();
-        return PIC_E_NODEVICE;
-    }
-    int dev = 0;
-    hipDeviceProp_t prop;
-    if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
-        (void)hipGetLastError();
-        return PIC_E_NODEVICE;
-    }
-    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-        return PIC_E_NODEVICE;
+    int32_t variant = 0;
+    st = resolve_variant(desc, &variant);
+    if (st != PIC_OK)
+        return st;
+    int dev = 0, num_cus = 0;
+    st = current_device(&dev);
+    if (st == PIC_OK)
+        st = gfx950_cus(dev, &num_cus);
+    if (st != PIC_OK)
+        return st;
 
     pic_decoder *d = new (std::nothrow) pic_decoder;
     if (!d)
         return PIC_E_NOMEM;
-    memset(d, 0, sizeof *d);
-    d->desc = *desc;
-    d->variant = variant;
-    d->device = dev;
-    d->num_cus = prop.multiProcessorCount;
-    for (int l = 0; l < nl; ++l) {
-        d->weights_per_image += (int64_t)desc->widths[l] * desc->widths[l + 1];
-        d->biases_per_image += desc->widths[l + 1];
-    }
+    init_handle(d, desc, variant, dev, num_cus);
     const size_t ctr_bytes = sizeof(int32_t) * 2 * (size_t)pic::tile_counters(desc->max_batch);
     void *mem = nullptr;
     if (hipMalloc(&mem, ctr_bytes) != hipSuccess || hipMemset(mem, 0, ctr_bytes) != hipSuccess ||
@@ -190,54 +232,12 @@ pic_status prepare(const pic_decoder *dec, int32_t batch, const float *const *la
     return PIC_OK;
 }
 
-pic_status launch(pic_decoder *dec, const pic::DecodeParams &params, void *stream)
+// The checks of pic_decode_run and the rest of its kernel argument.  PIC_OK
+// with nothing to enqueue when batch is 0.
+pic_status run_params(const pic_decoder *dec, int32_t batch, const float *const *latents, const void *weights,
+                      int64_t weights_img_stride, const float *biases, int64_t biases_img_stride, void *out,
+                      pic::DecodeParams &p)
 {
-    int cur = -1;
-    if (hipGetDevice(&cur) != hipSuccess || cur != dec->device) {
-        (void)hipGetLastError();
-        return PIC_E_INVALID;   // the handle belongs to another device
-    }
-    // this run's tile counters (cleared by the previous run, or at create)
-    // and the next run's (cleared by this one)
-    pic::DecodeParams p = params;
-    const int32_t mb = pic::tile_counters(dec->desc.max_batch);
-    p.tile_ctr = dec->d_ctr + (dec->runs & 1u) * mb;
-    p.tile_ctr_next = dec->d_ctr + ((dec->runs + 1u) & 1u) * mb;
-    p.tile_ctr_len = mb;
-    hipStream_t s = (hipStream_t)stream;
-    const char *name = nullptr;
-    int pxs = 0;
-    hipError_t e = hipErrorInvalidValue;
-    switch (dec->variant) {
-    case PIC_VARIANT_VALU: e = pic::launch_valu(p, s, &name, &pxs); break;
-    case PIC_VARIANT_MFMA_F32: e = pic::launch_mfma_f32(p, s, &name, &pxs, dec->num_cus); break;
-    case PIC_VARIANT_MFMA_BF16: e = pic::launch_mfma_bf16(p, s, &name, &pxs, dec->num_cus); break;
-    case PIC_VARIANT_MFMA_F16X3: e = pic::launch_mfma_f16x3(p, s, &name, &pxs, dec->num_cus); break;
-    }
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return PIC_E_HIP;
-    }
-    if (dec->variant != PIC_VARIANT_VALU)
-        ++dec->runs;
-    if (name) {
-        strncpy(dec->kernel_name, name, sizeof dec->kernel_name - 1);
-        dec->px_per_step = pxs;
-    }
-    return PIC_OK;
-}
-
-}  // namespace
-
-extern "C" {
-
-pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *latents,
-                          const void *weights, int64_t weights_img_stride,
-                          const float *biases, int64_t biases_img_stride,
-                          void *out, void *stream)
-{
-    if (!dec)
-        return PIC_E_INVALID;
     const pic_decode_desc &d = dec->desc;
     if (batch < 0 || batch > d.max_batch)
         return PIC_E_INVALID;
@@ -255,7 +255,6 @@ pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *l
         return PIC_E_INVALID;
     if (biases_img_stride != 0 && biases_img_stride < dec->biases_per_image)
         return PIC_E_INVALID;
-    pic::DecodeParams p;
     pic_status st = prepare(dec, batch, latents, out, p);
     if (st != PIC_OK)
         return st;
@@ -268,7 +267,156 @@ pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *l
         wo += (int64_t)d.widths[l] * d.widths[l + 1];
         bo += d.widths[l + 1];
     }
-    return launch(dec, p, stream);
+    return PIC_OK;
+}
+
+__global__ void k_clear_counters(int32_t *c, int n)
+{
+    for (int i = threadIdx.x; i < n; i += blockDim.x)
+        c[i] = 0;
+}
+
+// Enqueue the decode.  A handle's run uses one of its two counter slots
+// (cleared by the previous run, or at create) and has the kernel clear the
+// other.  With clear_here (pic_decode_run_noalloc: dec->d_ctr is one slot of
+// the library's per-device array, whose contents the previous call left), a
+// fill kernel clears the counters on the stream first and the decode kernel
+// clears nothing.
+pic_status launch(pic_decoder *dec, const pic::DecodeParams &params, void *stream, bool clear_here)
+{
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != dec->device) {
+        (void)hipGetLastError();
+        return PIC_E_INVALID;   // the handle belongs to another device
+    }
+    pic::DecodeParams p = params;
+    hipStream_t s = (hipStream_t)stream;
+    if (clear_here) {
+        p.tile_ctr = dec->d_ctr;
+        p.tile_ctr_next = dec->d_ctr;
+        p.tile_ctr_len = 0;
+        if (dec->variant != PIC_VARIANT_VALU) {   // (the reference family takes no tiles)
+            hipLaunchKernelGGL(k_clear_counters, dim3(1), dim3(256), 0, s, dec->d_ctr,
+                               pic::tile_counters(params.batch));
+            if (hipGetLastError() != hipSuccess)
+                return PIC_E_HIP;
+        }
+    } else {
+        const int32_t mb = pic::tile_counters(dec->desc.max_batch);
+        p.tile_ctr = dec->d_ctr + (dec->runs & 1u) * mb;
+        p.tile_ctr_next = dec->d_ctr + ((dec->runs + 1u) & 1u) * mb;
+        p.tile_ctr_len = mb;
+    }
+    const char *name = nullptr;
+    int pxs = 0;
+    hipError_t e = hipErrorInvalidValue;
+    switch (dec->variant) {
+    case PIC_VARIANT_VALU: e = pic::launch_valu(p, s, &name, &pxs); break;
+    case PIC_VARIANT_MFMA_F32: e = pic::launch_mfma_f32(p, s, &name, &pxs, dec->num_cus); break;
+    case PIC_VARIANT_MFMA_BF16: e = pic::launch_mfma_bf16(p, s, &name, &pxs, dec->num_cus); break;
+    case PIC_VARIANT_MFMA_F16X3: e = pic::launch_mfma_f16x3(p, s, &name, &pxs, dec->num_cus); break;
+    }
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return PIC_E_HIP;
+    }
+    if (dec->variant != PIC_VARIANT_VALU && !clear_here)
+        ++dec->runs;
+    if (name) {
+        strncpy(dec->kernel_name, name, sizeof dec->kernel_name - 1);
+        dec->px_per_step = pxs;
+    }
+    return PIC_OK;
+}
+
+// Per-device state of pic_decode_run_noalloc, set up on its first call on a
+// device (with that device current): the device address of `scratch` and the
+// compute-unit count.
+constexpr int kMaxDevices = 64;
+struct NoAllocDevice {
+    bool ready;
+    pic_status status;     // of the set-up (PIC_OK, PIC_E_NODEVICE or PIC_E_HIP)
+    int32_t *scratch;      // device address of this device's copy of `scratch`
+    int num_cus;
+};
+std::mutex g_noalloc_mu;
+NoAllocDevice g_noalloc[kMaxDevices];
+
+pic_status noalloc_state(int dev, NoAllocDevice *out)
+{
+    if (dev < 0 || dev >= kMaxDevices)
+        return PIC_E_NODEVICE;
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    NoAllocDevice &st = g_noalloc[dev];
+    if (!st.ready) {
+        st.status = gfx950_cus(dev, &st.num_cus);
+        if (st.status == PIC_OK) {
+            void *ptr = nullptr;
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+                (void)hipGetLastError();
+                st.status = PIC_E_HIP;
+            } else {
+                st.scratch = static_cast<int32_t *>(ptr);
+            }
+        }
+        st.ready = true;
+    }
+    *out = st;
+    return st.status;
+}
+
+}  // namespace
+
+extern "C" {
+
+pic_status pic_decode_run(pic_decoder *dec, int32_t batch, const float *const *latents,
+                          const void *weights, int64_t weights_img_stride,
+                          const float *biases, int64_t biases_img_stride,
+                          void *out, void *stream)
+{
+    if (!dec)
+        return PIC_E_INVALID;
+    pic::DecodeParams p;
+    const pic_status st = run_params(dec, batch, latents, weights, weights_img_stride, biases,
+                                     biases_img_stride, out, p);
+    if (st != PIC_OK || batch == 0)
+        return st;
+    return launch(dec, p, stream, false);
+}
+
+pic_status pic_decode_run_noalloc(const pic_decode_desc *desc, int32_t batch, const float *const *latents,
+                                  const void *weights, int64_t weights_img_stride,
+                                  const float *biases, int64_t biases_img_stride,
+                                  void *out, void *stream)
+{
+    pic_status st = validate_desc(desc);
+    if (st != PIC_OK)
+        return st;
+    if (batch > PIC_NOALLOC_MAX_BATCH && batch <= desc->max_batch)
+        return PIC_E_UNSUPPORTED;    // beyond the library's counter array
+    int32_t variant = 0;
+    st = resolve_variant(desc, &variant);
+    if (st != PIC_OK)
+        return st;
+    // a handle on the stack: host fields only, its counters the array's
+    pic_decoder dec;
+    init_handle(&dec, desc, variant, 0, 0);
+    pic::DecodeParams p;
+    st = run_params(&dec, batch, latents, weights, weights_img_stride, biases, biases_img_stride, out, p);
+    if (st != PIC_OK || batch == 0)
+        return st;
+    int dev = 0;
+    st = current_device(&dev);
+    if (st != PIC_OK)
+        return st;
+    NoAllocDevice nd;
+    st = noalloc_state(dev, &nd);
+    if (st != PIC_OK)
+        return st;
+    dec.device = dev;
+    dec.num_cus = nd.num_cus;
+    dec.d_ctr = nd.scratch;
+    return launch(&dec, p, stream, true);
 }
 
 pic_status pic_decode_run_layers(pic_decoder *dec, int32_t batch, const float *const *latents,
@@ -306,7 +454,7 @@ pic_status pic_decode_run_layers(pic_decoder *dec, int32_t batch, const float *c
         p.bl[l] = layer_biases[l];
         p.bls[l] = layer_bias_strides[l];
     }
-    return launch(dec, p, stream);
+    return launch(dec, p, stream, false);
 }
 
 pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *info)

@@ -24,6 +24,7 @@ PIC_OK, PIC_E_INVALID, PIC_E_UNSUPPORTED, PIC_E_NODEVICE, PIC_E_HIP, PIC_E_NOMEM
 PIC_F32, PIC_BF16, PIC_U8 = 0, 1, 2
 PIC_VARIANT_AUTO, PIC_VARIANT_VALU, PIC_VARIANT_MFMA_F32, PIC_VARIANT_MFMA_BF16, PIC_VARIANT_MFMA_F16X3 = range(5)
 PIC_MAX_LEVELS, PIC_MAX_LAYERS, PIC_MAX_WIDTH, PIC_MAX_BATCH = 12, 8, 128, 65535
+PIC_NOALLOC_MAX_BATCH = 4096
 PIC_FLAG_NO_CLAMP = 1
 
 VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,
@@ -32,8 +33,8 @@ VARIANTS = {"auto": PIC_VARIANT_AUTO, "valu": PIC_VARIANT_VALU,
 VARIANT_NAMES = {v: k for k, v in VARIANTS.items()}
 
 # Every symbol include/pic_decode.h and include/pic_zpr.h declare.
-EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_run_layers", "pic_decode_query",
-           "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation",
+EXPORTS = ("pic_decode_create", "pic_decode_run", "pic_decode_run_noalloc", "pic_decode_run_layers",
+           "pic_decode_query", "pic_decode_destroy", "pic_status_string", "pic_fuse_modulation",
            "pic_zpr_create", "pic_zpr_decode", "pic_zpr_expand", "pic_zpr_query", "pic_zpr_destroy",
            "pic_huff_create", "pic_huff_decode", "pic_huff_query", "pic_huff_destroy")
 
@@ -105,6 +106,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pic_decode_run.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
                                    ctypes.c_void_p, ctypes.c_void_p]
+    lib.pic_decode_run_noalloc.restype = ctypes.c_int
+    lib.pic_decode_run_noalloc.argtypes = [ctypes.POINTER(pic_decode_desc), ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                           ctypes.c_void_p, ctypes.c_void_p]
     lib.pic_decode_run_layers.restype = ctypes.c_int
     lib.pic_decode_run_layers.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -184,6 +189,16 @@ def pic_decode_run(handle: int, batch: int, latent_ptrs: Sequence[int], weights_
     return load_library().pic_decode_run(handle, batch, arr if latent_ptrs is not None else None,
                                          weights_ptr, weights_img_stride, biases_ptr,
                                          biases_img_stride, out_ptr, stream)
+
+
+def pic_decode_run_noalloc(desc: pic_decode_desc, batch: int, latent_ptrs: Sequence[int], weights_ptr: int,
+                           weights_img_stride: int, biases_ptr: int, biases_img_stride: int,
+                           out_ptr: int, stream: int = 0) -> int:
+    """Raw-pointer call of the entry point that allocates nothing (no handle:
+    the descriptor is passed each time); returns the status."""
+    arr = (ctypes.c_void_p * max(1, len(latent_ptrs)))(*latent_ptrs)
+    return load_library().pic_decode_run_noalloc(ctypes.byref(desc), batch, arr, weights_ptr, weights_img_stride,
+                                                 biases_ptr, biases_img_stride, out_ptr, stream)
 
 
 def pic_decode_run_layers(handle: int, batch: int, latent_ptrs: Sequence[int], layer_weight_ptrs: Sequence[int],
