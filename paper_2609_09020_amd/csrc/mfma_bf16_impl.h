@@ -4,10 +4,10 @@
 // Same computation and tiling as the fp32 family (PIC, Sec. 3.1 and App. A;
 // tiles, LDS boxes and upsample in decode_common.h), with the MLP weights
 // given in bfloat16.  The weights are used exactly; every activation h fed to
-// a matrix core is split into two bfloat16 numbers, hi = h with the low 16
-// mantissa bits cleared and lo = round-to-nearest-even(h - hi), and each
-// product is formed as W * hi + W * lo (two MFMAs into one fp32
-// accumulator).  |h - hi - lo| <= 2^-16 |h|, so the split costs about as
+// a matrix core is split into two bfloat16 numbers, hi = RNE_bf16(h) and
+// lo = RNE_bf16(h - hi), and each product is formed as W * hi + W * lo (two
+// MFMAs into one fp32 accumulator).  |h - hi| <= 2^-8 |h| and
+// |h - hi - lo| <= 2^-8 |h - hi| <= 2^-16 |h|, so the split costs about as
 // much accuracy as binary32 rounding of a short dot product, not bfloat16's.
 //
 // Matrix-core mapping (lane l, lane group g = l / 16, i = l % 16)
@@ -18,7 +18,11 @@
 //   2s and 2s+1: K index 8g + j is neuron 16 (2s + j / 4) + 4g + j % 4, which
 //   the lane already holds (registers j % 4 of blocks 2s + j / 4).  The
 //   weights are laid out to match.  For the first layer, lane group g carries
-//   levels LPG g + j (j < LPG = ceil(L / 4)) at K indices 8g + j.
+//   levels LPG g + j (j < LPG = ceil(L / 4)), hi and lo parts both, in one K
+//   step: K word w (indices 8g + 2w, 8g + 2w + 1) holds the hi parts of
+//   levels 2p, 2p + 1 for w = 2p, their lo parts for w = 2p + 1, and for odd
+//   LPG the last level's (hi, lo) in word LPG - 1; the weights repeat to
+//   match, so one MFMA per block forms W * hi + W * lo.
 //   Biases start the accumulators; the output layer (3 neurons) runs in fp32
 //   on the vector ALU as in the fp32 family.
 #pragma once
@@ -48,17 +52,38 @@ struct Layout {
 };
 
 // (x0, x1) -> {hi, lo}: the packed bfloat16 pairs (hi0, hi1) and (lo0, lo1),
-// low halves first.
+// low halves first.  hi = RNE_bf16(x); the remainder x - hi is formed by one
+// dot product per value, hi . (-1, -0) + x0 and hi . (-0, -1) + x1 (exact:
+// the products are exact and the result is representable in binary32), and
+// rounded by one packed conversion: 4 instructions per pair.
 __device__ __forceinline__ u32x2 split_pair(float x0, float x1)
 {
-    const unsigned b0 = __float_as_uint(x0), b1 = __float_as_uint(x1);
-    // the high halves of b0 and b1, in one byte permute
-    const unsigned hi = __builtin_amdgcn_perm(b1, b0, 0x07060302u);
-    const float r0 = x0 - __uint_as_float(b0 & 0xffff0000u);
-    const float r1 = x1 - __uint_as_float(b1 & 0xffff0000u);
-    // both remainders rounded to bfloat16 by one packed conversion
-    const bf16x2 l = __builtin_convertvector((f32x2{r0, r1}), bf16x2);
-    return u32x2{hi, __builtin_bit_cast(unsigned, l)};
+    const bf16x2 hi = __builtin_convertvector((f32x2{x0, x1}), bf16x2);
+    // (-1, -0) and (-0, -1), not (-1, 0): the compiler would encode (-1, 0)
+    // as the inline constant -1.0, which the instruction does not read as
+    // that bf16 pair; these two stay 32-bit literals.  -0 * hi adds nothing.
+    const bf16x2 neg_lo = {(__bf16)-1.0f, (__bf16)-0.0f}, neg_hi = {(__bf16)-0.0f, (__bf16)-1.0f};
+    const float r0 = __builtin_amdgcn_fdot2_f32_bf16(hi, neg_lo, x0, false);
+    const float r1 = __builtin_amdgcn_fdot2_f32_bf16(hi, neg_hi, x1, false);
+    const bf16x2 lo = __builtin_convertvector((f32x2{r0, r1}), bf16x2);
+    return u32x2{__builtin_bit_cast(unsigned, hi), __builtin_bit_cast(unsigned, lo)};
+}
+
+// x -> the packed pair (hi, lo) of one value, as split_pair computes them.
+__device__ __forceinline__ unsigned split_one(float x)
+{
+    const bf16x2 h = __builtin_convertvector((f32x2{x, 0.0f}), bf16x2);
+    const bf16x2 neg_lo = {(__bf16)-1.0f, (__bf16)-0.0f};
+    const float r = __builtin_amdgcn_fdot2_f32_bf16(h, neg_lo, x, false);
+    return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2{x, r}), bf16x2));
+}
+
+// Level j (< LPG) of a lane group behind half h of first-layer K word w, or
+// -1 for an empty slot (the word order of the hi/lo packing above).
+template <int LPG>
+__host__ __device__ constexpr int l1_level(int w, int h)
+{
+    return w < 2 * (LPG / 2) ? 2 * (w / 2) + h : (w == LPG - 1 && (LPG & 1) ? LPG - 1 : -1);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -66,7 +91,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LPG: levels
 // per lane group in the first layer (ceil(L / 4)).
 template <int NB, int NH, int LPG>
-__global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int blocks_per_image,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <= 2 ? 4 : 1))) void k_mfma_bf16(DecodeParams p, int blocks_per_image,
                                                         int tiles_x, int tiles)
 {
     using LY = Layout<NB, NH, LPG>;
@@ -106,8 +131,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
             unsigned w = 0;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int j = 2 * u + h, lvl = LPG * gg + j;
-                if (j < LPG && lvl < L && out < N1)
+                const int j = l1_level<LPG>(u, h), lvl = LPG * gg + j;
+                if (j >= 0 && lvl < L && out < N1)
                     w |= l0.bits(out * L + lvl) << (16 * h);
             }
             return w;
@@ -163,18 +188,6 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
         store_boxes<4 * LPG>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
-    u32x4 w1[NB];
-#pragma unroll
-    for (int ob = 0; ob < NB; ++ob)
-        w1[ob] = *reinterpret_cast<const u32x4 *>(&ldsu[LY::W1A + (ob * 64 + lane) * 4]);
-    u32x4 wh[NH > 0 ? NH : 1][NB][KS2];
-#pragma unroll
-    for (int hl = 0; hl < NH; ++hl)
-#pragma unroll
-        for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-            for (int st = 0; st < KS2; ++st)
-                wh[hl][ob][st] = *reinterpret_cast<const u32x4 *>(&ldsu[LY::WHA + (((hl * NB + ob) * KS2 + st) * 64 + lane) * 4]);
 
     // ---- the levels this lane samples: LPG g + j, j < LPG (level 0 where the
     // level does not exist; its weights are zero).
@@ -236,27 +249,27 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                 asm volatile("" ::: "memory");
 
                 // layer 1: B operand = the lane's LPG upsampled levels, split
-                float u[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                // and packed hi and lo into one K step
+                float u[LPG];
 #pragma unroll
                 for (int j = 0; j < LPG; ++j)
                     u[j] = lane_level_sample(lds, lv[j], roff[j], rly[j], cg);
-                u32x4 bh = {0u, 0u, 0u, 0u}, bl = {0u, 0u, 0u, 0u};
-                {
-                    const u32x2 q = split_pair(u[0], u[1]);
-                    bh[0] = q[0];
-                    bl[0] = q[1];
+                u32x4 bx = {0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int j = 0; j + 1 < LPG; j += 2) {
+                    const u32x2 q = split_pair(u[j], u[j + 1]);
+                    bx[j] = q[0];
+                    bx[j + 1] = q[1];
                 }
-                if (LPG > 2) {
-                    const u32x2 q = split_pair(u[2], u[3]);
-                    bh[1] = q[0];
-                    bl[1] = q[1];
-                }
+                if (LPG & 1)
+                    bx[LPG - 1] = split_one(u[LPG - 1]);
                 f32x4 d[NB];
 #pragma unroll
                 for (int ob = 0; ob < NB; ++ob) {
+                    // (A operands read from LDS per group, like the hidden layers')
+                    const u32x4 w1 = *reinterpret_cast<const u32x4 *>(&ldsu[LY::W1A + (ob * 64 + lane) * 4]);
                     d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + (ob * 64 + lane) * 4]);
-                    d[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1[ob]), as_bf16x8(bh), d[ob], 0, 0, 0);
-                    d[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1[ob]), as_bf16x8(bl), d[ob], 0, 0, 0);
+                    d[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1), as_bf16x8(bx), d[ob], 0, 0, 0);
                 }
 #pragma unroll
                 for (int ob = 0; ob < NB; ++ob)
@@ -287,15 +300,24 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
                         e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BH + ((hl * NB + ob) * 64 + lane) * 4]);
+                    // A operands from LDS (16 bytes per lane per block and K
+                    // step), read per group: held in VGPRs they would cost a
+                    // wavefront per SIMD
 #pragma unroll
-                    for (int st = 0; st < KS2; ++st)
+                    for (int st = 0; st < KS2; ++st) {
+                        u32x4 wa[NB];
+#pragma unroll
+                        for (int ob = 0; ob < NB; ++ob)
+                            wa[ob] = *reinterpret_cast<const u32x4 *>(
+                                &ldsu[LY::WHA + (((hl * NB + ob) * KS2 + st) * 64 + lane) * 4]);
 #pragma unroll
                         for (int ob = 0; ob < NB; ++ob) {
-                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wh[hl][ob][st]),
-                                                                            as_bf16x8(xh[st]), e[ob], 0, 0, 0);
-                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wh[hl][ob][st]),
-                                                                            as_bf16x8(xl[st]), e[ob], 0, 0, 0);
+                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wa[ob]), as_bf16x8(xh[st]), e[ob],
+                                                                            0, 0, 0);
+                            e[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wa[ob]), as_bf16x8(xl[st]), e[ob],
+                                                                            0, 0, 0);
                         }
+                    }
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob)
 #pragma unroll
@@ -303,21 +325,24 @@ __global__ __launch_bounds__(kThreads) void k_mfma_bf16(DecodeParams p, int bloc
                             d[ob][r] = relu(e[ob][r]);
                 }
 
-                // output layer on the vector ALU (fp32); a block's four weight
-                // reads are issued before their first use, so one LDS round
-                // trip covers them
+                // output layer on the vector ALU (fp32); weight reads are issued
+                // two at a time before their first use (four at a time cost
+                // the wider shapes a wavefront per SIMD)
                 float o0 = ob0, o1 = ob1, o2 = ob2;
 #pragma unroll
                 for (int ob = 0; ob < NB; ++ob) {
-                    f32x4 w3[4];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        w3[r] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((ob * 4 + r) * 4 + g) * 4]);
+                    for (int r0 = 0; r0 < 4; r0 += 2) {
+                        f32x4 w3[2];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        o0 = __builtin_fmaf(w3[r][0], d[ob][r], o0);
-                        o1 = __builtin_fmaf(w3[r][1], d[ob][r], o1);
-                        o2 = __builtin_fmaf(w3[r][2], d[ob][r], o2);
+                        for (int r = 0; r < 2; ++r)
+                            w3[r] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + ((ob * 4 + r0 + r) * 4 + g) * 4]);
+#pragma unroll
+                        for (int r = 0; r < 2; ++r) {
+                            o0 = __builtin_fmaf(w3[r][0], d[ob][r0 + r], o0);
+                            o1 = __builtin_fmaf(w3[r][1], d[ob][r0 + r], o1);
+                            o2 = __builtin_fmaf(w3[r][2], d[ob][r0 + r], o2);
+                        }
                     }
                 }
                 const float v = row_sum3(o0, o1, o2);
