@@ -14,9 +14,10 @@ sample of the same workload (rank 0, N = 1 only).
 
 The same line carries `per_config`: every other workload of the benchmark
 suite (64x64; 768x512 x64; 2048x1536 x1 and x16; 3840x2160 with fp32 and
-with bf16 weights; the paper's 4-layer net at 768x512), each timed after the
-headline's timed region with HIP events over back-to-back launches, with its
-roofline fraction; and `paper_context`: the paper's own decoding speed with
+with bf16 weights; the paper's 4-layer net at 768x512; 768x512 and 3840x2160
+again in the fp16-split matrix-core family), each timed after the headline's
+timed region with HIP events over back-to-back launches, with its roofline
+fraction; and `paper_context`: the paper's own decoding speed with
 the hardware it was measured on (context, not the target).
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload kodak768]
@@ -183,6 +184,9 @@ PAPER_CONTEXT = {
 
 # Workloads of the benchmark suite timed beside the headline one (per_config).
 PER_CONFIG = ["pic64", "kodak768_b64", "clic2048", "clic2048_b16", "uhd4k", "uhd4k_bf16", "kodak768_paper"]
+# fp32-weight workloads also timed in the fp16-split matrix-core family (fp32
+# accuracy from fp16 matrix instructions): key "<workload>@mfma_f16x3"
+PER_CONFIG_F16X3 = ["kodak768", "uhd4k"]
 
 
 def time_workload(name, variant="auto", out_dtype="f32", target_s=0.3):
@@ -242,8 +246,8 @@ def time_workload(name, variant="auto", out_dtype="f32", target_s=0.3):
 
 
 def peaks(args):
-    """Peak issue rates on this GPU (SURVEY-style microbenchmarks, used to
-    ground the design): fp32 / bf16 / fp16 matrix instructions and fp32 vector
+    """Peak issue rates on this GPU (microbenchmarks that ground the kernel
+    design): fp32 / bf16 / fp16 matrix instructions and fp32 vector
     FMAs, each with independent accumulators, the fp32 and bf16 matrix
     instructions interleaved with vector FMAs in the same wavefronts, and a
     device-to-device copy.  One JSON line per measurement."""
@@ -310,7 +314,9 @@ def peaks(args):
 def width_sweep(args):
     """Decode speed against synthesis width for the paper's net shape: L = 8
     levels, three hidden layers of width W, 3 outputs, 768x512 (the Kodak image
-    size), fp32.  Width 8 runs in 16-wide matrix blocks (zero padded)."""
+    size), fp32, in the fp32 matrix-core, fp16-split matrix-core and vector
+    families.  Width 8 runs in 16-wide matrix blocks (zero padded)."""
+    import ctypes
     import torch
     from paper_2609_09020_amd import synth
     from paper_2609_09020_amd import decoder as D
@@ -324,10 +330,23 @@ def width_sweep(args):
         lat = [torch.from_numpy(a).to(dev) for a in inp.latents]
         wt = torch.from_numpy(inp.weights).to(dev)
         bt = torch.from_numpy(inp.biases).to(dev)
-        for variant in ("mfma_f32", "valu"):
+        lib = D.load_library()
+        lat_arr = (ctypes.c_void_p * len(lat))(*[t.data_ptr() for t in lat])
+        for variant in ("mfma_f32", "mfma_f16x3", "valu"):
             dec = D.Decoder(H, W, widths, max_batch=1, variant=variant)
             out = dec.alloc_out(1, dev)
-            ms, wall = time_calls(lambda: dec.run(lat, wt, bt, out=out), args.steps, args.warmup, stream)
+            # the pre-marshalled raw call, as in the main measurement: the
+            # Python wrapper's checks would make a call of this size host-bound
+            run_args = (ctypes.c_void_p(dec.handle), ctypes.c_int32(1), lat_arr,
+                        ctypes.c_void_p(wt.data_ptr()), ctypes.c_int64(dec.nw),
+                        ctypes.c_void_p(bt.data_ptr()), ctypes.c_int64(dec.nb),
+                        ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+
+            def run():
+                st = lib.pic_decode_run(*run_args)
+                if st != D.PIC_OK:
+                    raise D.PicError(st, "pic_decode_run")
+            ms, wall = time_calls(run, args.steps, args.warmup, stream)
             fpp = flops_per_pixel(widths)
             print(json.dumps({"sweep": "width", "widths": list(widths), "variant": variant,
                               "kernel_avg_ms": round(ms, 5), "mpixel_s": round(H * W / ms / 1e3, 1),
@@ -701,6 +720,9 @@ def main():
     if not args.no_per_config:
         res["per_config"] = {name: time_workload(name, out_dtype=args.out_dtype)
                              for name in PER_CONFIG if name != args.workload}
+        for name in PER_CONFIG_F16X3:
+            res["per_config"][f"{name}@mfma_f16x3"] = time_workload(name, variant="mfma_f16x3",
+                                                                    out_dtype=args.out_dtype)
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, inp)
