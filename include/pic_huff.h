@@ -49,9 +49,14 @@ enum {
     PIC_HUFF_ERR_BITS = 1,          /* the bits end before n_symbols codewords      */
     PIC_HUFF_ERR_CODE = 2,          /* a bit pattern that starts no codeword; the
                                        decoding stops there (BITS is then not set)  */
-    PIC_HUFF_ERR_TABLE = 4          /* a length outside 1 .. PIC_HUFF_MAX_LEN, or an
+    PIC_HUFF_ERR_TABLE = 4,         /* a length outside 1 .. PIC_HUFF_MAX_LEN, or an
                                        over-subscribed code (Kraft sum above 1);
                                        nothing is decoded                           */
+    PIC_HUFF_ERR_SYNC = 8           /* a short stream's one-launch decode: a
+                                       workgroup gave up waiting (a bounded wait,
+                                       about 0.2 s) for the repair step of the
+                                       others; its symbols are not written. Calls
+                                       on one handle must not overlap           */
 };
 
 /* Zero-initialise, then set struct_size = sizeof(pic_huff_desc). */
@@ -95,9 +100,14 @@ PIC_API pic_status pic_huff_create(const pic_huff_desc *desc, pic_huff **out);
  *               need to clear it first; readable after the stream reaches it).
  *   stream    : hipStream_t (NULL: the null stream).
  * `values`, `out` and `status` must be 4-byte aligned; buffers must not
- * overlap.  Asynchronous: no allocation, no synchronisation.  Returns
- * PIC_E_INVALID for a bad argument (nothing enqueued), PIC_E_HIP for a
- * failed launch.
+ * overlap.  Asynchronous: no allocation, no synchronisation.  A stream of up
+ * to 64 * 255 * 64 bits (about 1 Mbit: one Kodak-size image) is decoded in
+ * one launch of at most 64 workgroups that hand the repair step to the last
+ * of them; the others wait for it at most about 0.2 s (PIC_HUFF_ERR_SYNC:
+ * only when other work keeps some of the 64 from starting that long).  A
+ * longer stream takes three launches.  Calls on one handle share its
+ * scratch and must not overlap.  Returns PIC_E_INVALID for a bad argument
+ * (nothing enqueued), PIC_E_HIP for a failed launch.
  */
 PIC_API pic_status pic_huff_decode(pic_huff *h, const uint8_t *data, int64_t n_bits, const int32_t *values,
                                    const uint8_t *lengths, int32_t n_table, int64_t n_symbols, int32_t *out,

@@ -15,7 +15,7 @@ struct pic_huff {
     int64_t scratch_bytes;
     char *d_scratch;
     // offsets of the scratch arrays
-    size_t o_mask, o_end, o_cnt, o_fail, o_flags, o_blk, o_bnd;
+    size_t o_mask, o_end, o_cnt, o_fail, o_flags, o_blk, o_bnd, o_sync;
 };
 
 namespace {
@@ -76,6 +76,7 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
     h->o_flags = o;  o += align256(sizeof(int32_t) * 4);
     h->o_blk = o;    o += align256(sizeof(int32_t) * nblk);
     h->o_bnd = o;    o += align256(sizeof(int32_t) * nblk);
+    h->o_sync = o;   o += align256(sizeof(uint64_t));
     h->scratch_bytes = (int64_t)o;
     void *mem = nullptr;
     if (hipMalloc(&mem, o) != hipSuccess) {
@@ -84,6 +85,15 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
         return PIC_E_HIP;
     }
     h->d_scratch = static_cast<char *>(mem);
+    // the one-launch path's hand-off word starts at zero; each launch leaves
+    // it ready for the next
+    if (hipMemset(h->d_scratch + h->o_sync, 0, sizeof(uint64_t)) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(mem);
+        delete h;
+        return PIC_E_HIP;
+    }
     *out = h;
     return PIC_OK;
 }
@@ -129,6 +139,8 @@ pic_status pic_huff_decode(pic_huff *h, const uint8_t *data, int64_t n_bits, con
     p.bnd = reinterpret_cast<int32_t *>(h->d_scratch + h->o_bnd);
     p.nblk = (p.nsub + pic::kHuffOwn - 1) / pic::kHuffOwn;
     p.blk_is_prefix = p.nblk > pic::kHuffPrefixInKernelMax;
+    p.sync = reinterpret_cast<uint64_t *>(h->d_scratch + h->o_sync);
+    p.spin_limit = pic::kHuffSpinLimit;
     if (pic::launch_huff(p, (hipStream_t)stream) != hipSuccess) {
         (void)hipGetLastError();
         return PIC_E_HIP;

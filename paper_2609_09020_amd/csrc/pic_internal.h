@@ -133,6 +133,8 @@ constexpr int kHuffPrefixInKernelMax = 4096;   // more workgroups: the fix kerne
 constexpr int kHuffLutBits = 11;               // first-level decode table: 2^11 entries
 constexpr int kHuffMaxLen = 24;
 constexpr int kHuffMaxTable = 4096;
+constexpr int kHuffOneLaunchMax = 64;          // workgroups: one launch (parse, repair, write)
+constexpr uint32_t kHuffSpinLimit = 1u << 22;  // polls of 128 cycles: about 0.2 s
 
 // Kernel argument of the entropy-decoding kernels.
 struct HuffParams {
@@ -160,6 +162,9 @@ struct HuffParams {
                                     // moved; bit 1: the workgroup left subsequences to the fix kernel
     int32_t nblk;                   // workgroups of the parse and write kernels
     int32_t blk_is_prefix;
+    uint64_t *sync;                 // [1]: the one-launch path's hand-off word (generation << 32 |
+                                    // arrivals), zero at create
+    uint32_t spin_limit;            // polls a workgroup waits for the repair step at most
 };
 
 hipError_t launch_huff(const HuffParams &p, hipStream_t s);
