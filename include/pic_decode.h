@@ -254,8 +254,11 @@ PIC_API pic_status pic_decode_query(const pic_decoder *dec, pic_decode_info *inf
  * accepted).  Synchronises the handle's device first. */
 PIC_API void pic_decode_destroy(pic_decoder *dec);
 
-/* pic_status_string -- static description of a status code (never NULL). */
-PIC_API const char *pic_status_string(pic_status s);
+/* pic_status_string -- static description of a status code (never NULL).
+ * `status` is a pic_status value; any other int32_t gives "unknown status"
+ * (the parameter is an int32_t so that a value outside the enumeration is
+ * well defined to pass). */
+PIC_API const char *pic_status_string(int32_t status);
 
 #ifdef __cplusplus
 }

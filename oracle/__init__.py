@@ -277,12 +277,18 @@ _default = None
 
 
 def default() -> Oracle:
-    """The oracle built from oracle/pic_oracle.c (built on first use)."""
+    """The oracle built from oracle/pic_oracle.c (built on first use).  The
+    environment variable PIC_ORACLE_LIB names another build of the same
+    sources to use instead (the sanitizer test's)."""
     global _default
     if _default is None:
-        if not os.path.exists(_build.LIB):
-            _build.build()
-        _default = Oracle(_build.LIB)
+        alt = os.environ.get("PIC_ORACLE_LIB")
+        if alt:
+            _default = Oracle(alt)
+        else:
+            if not os.path.exists(_build.LIB):
+                _build.build()
+            _default = Oracle(_build.LIB)
     return _default
 
 

@@ -18,12 +18,12 @@ SRCS = (SRC, ZPR_SRC, HUFF_SRC)
 LIB = os.path.join(HERE, "libpic_oracle.so")
 
 
-def build(verbose: bool = False, srcs=SRCS, out: str = LIB) -> str:
+def build(verbose: bool = False, srcs=SRCS, out: str = LIB, extra_flags=()) -> str:
     """Compile the C files ``srcs`` (default: the oracle's) into the shared
-    library ``out``."""
+    library ``out``; ``extra_flags`` go to gcc as well (e.g. sanitizers)."""
     tmp = out + f".tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-           "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, *srcs, "-lm"]
+           "-fPIC", "-shared", "-Wall", "-Wextra", *extra_flags, "-o", tmp, *srcs, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

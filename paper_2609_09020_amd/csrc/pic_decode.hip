@@ -139,9 +139,9 @@ void init_handle(pic_decoder *d, const pic_decode_desc *desc, int32_t variant, i
 
 extern "C" {
 
-const char *pic_status_string(pic_status s)
+const char *pic_status_string(int32_t status)
 {
-    switch (s) {
+    switch (status) {
     case PIC_OK: return "ok";
     case PIC_E_INVALID: return "invalid argument";
     case PIC_E_UNSUPPORTED: return "unsupported configuration";

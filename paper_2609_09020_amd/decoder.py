@@ -124,7 +124,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pic_decode_destroy.restype = None
     lib.pic_decode_destroy.argtypes = [ctypes.c_void_p]
     lib.pic_status_string.restype = ctypes.c_char_p
-    lib.pic_status_string.argtypes = [ctypes.c_int]
+    lib.pic_status_string.argtypes = [ctypes.c_int32]
     lib.pic_zpr_create.restype = ctypes.c_int
     lib.pic_zpr_create.argtypes = [ctypes.POINTER(pic_zpr_desc), ctypes.POINTER(ctypes.c_void_p)]
     for name in ("pic_zpr_decode", "pic_zpr_expand"):
