@@ -16,10 +16,19 @@
 // that holds a CU while others of the launch wait for one could wait for
 // ever, so a waiter stops after `spin_limit` polls and reports it.
 //
+// Leaving: a second word, error bits << 32 | departures, also zero at
+// create.  Every workgroup leaves once, after its last write, whatever path
+// it took (a waiter that gave up included): it ors its error bits into the
+// word, then counts itself; the last to leave receives every workgroup's
+// bits and resets the word.  Error bits of a waiter that gives up go this
+// way, not straight into the caller's status, which the launch's first
+// workgroup may clear later than the waiter gives up.
+//
 // The protocol is written once over an operations policy, so that the host
 // can run it with std::atomic and threads (its tests) and the kernel with
 // device-scope atomics:
 //   uint64_t Ops::fetch_add(uint64_t *w, uint64_t v)   returns the old value
+//   void     Ops::fetch_or(uint64_t *w, uint64_t v)
 //   uint64_t Ops::load(const uint64_t *w)
 //   void     Ops::store(uint64_t *w, uint64_t v)
 //   void     Ops::pause()                               between polls
@@ -72,6 +81,46 @@ PIC_HD inline bool wait(const uint64_t *word, const Arrival &a, uint32_t spin_li
     }
     return (uint32_t)(Ops::load(word) >> 32) != a.generation;
 }
+
+// Leave; one call per workgroup and launch, after its last write.  True for
+// the last to leave, which receives in *all_err the error bits every
+// workgroup left with (the word is then reset for the next launch).
+template <class Ops>
+PIC_HD inline bool leave(uint64_t *word, uint32_t n, uint32_t err, uint32_t *all_err)
+{
+    if (err)
+        Ops::fetch_or(word, (uint64_t)err << 32);
+    const uint64_t old = Ops::fetch_add(word, 1u);   // after the or: one location, one order
+    if ((uint32_t)old != n - 1u)
+        return false;
+    *all_err = (uint32_t)(old >> 32);
+    Ops::store(word, 0);
+    return true;
+}
+
+#if defined(__HIPCC__)
+// The kernels' policy: device-scope atomics on the scratch words (one
+// coherent place for every XCD), a short sleep between polls.
+struct DeviceOps {
+    __device__ static uint64_t fetch_add(uint64_t *w, uint64_t v)
+    {
+        return __hip_atomic_fetch_add(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ static void fetch_or(uint64_t *w, uint64_t v)
+    {
+        (void)__hip_atomic_fetch_or(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ static uint64_t load(const uint64_t *w)
+    {
+        return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ static void store(uint64_t *w, uint64_t v)
+    {
+        __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ static void pause() { __builtin_amdgcn_s_sleep(2); }
+};
+#endif
 
 }  // namespace huff_barrier
 }  // namespace pic

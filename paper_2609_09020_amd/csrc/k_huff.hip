@@ -880,22 +880,6 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
 // kernel that holds the CUs past the wait bound makes a waiter give up, and
 // every wait ends either way.  Records cross workgroups, and XCDs, through
 // device-scope release and acquire fences around the hand-off.
-struct DeviceOps {
-    __device__ static uint64_t fetch_add(uint64_t *w, uint64_t v)
-    {
-        return __hip_atomic_fetch_add(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __device__ static uint64_t load(const uint64_t *w)
-    {
-        return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __device__ static void store(uint64_t *w, uint64_t v)
-    {
-        __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __device__ static void pause() { __builtin_amdgcn_s_sleep(2); }
-};
-
 __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
 {
     warm_kernel_args<sizeof(HuffParams)>();
@@ -934,11 +918,16 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
         parse_phase(p, s_tab, s_words, s_u.parse.end, s_u.parse.moved, s_wsum, blk);
     }
     // hand-off: every workgroup arrives, also with an invalid table, so that
-    // the word's count comes back to zero
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    // the word's count comes back to zero.  Each wavefront waits for its
+    // record stores to reach the L2, then one write-back of the L2 publishes
+    // them all (one per workgroup, not one per wavefront).
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (l < 64)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (l == 0) {
-        const huff_barrier::Arrival a = huff_barrier::arrive<DeviceOps>(p.sync, (uint32_t)p.nblk);
+        const huff_barrier::Arrival a = huff_barrier::arrive<huff_barrier::DeviceOps>(p.sync, (uint32_t)p.nblk);
         s_last = a.last;
         s_gen = a.generation;
     }
@@ -947,28 +936,41 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
     a.generation = s_gen;
     a.last = s_last != 0;
     if (a.last) {                          // uniform
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // one invalidate per workgroup: its wavefronts share one CU
+        if (l < 64)
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __syncthreads();
         fix_phase(p, s_tab, valid, s_u.list, s_wsum);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (l < 64)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         __syncthreads();
         if (l == 0)
-            huff_barrier::release<DeviceOps>(p.sync, a);
+            huff_barrier::release<huff_barrier::DeviceOps>(p.sync, a);
     } else {
         if (l == 0)
-            s_ok = huff_barrier::wait<DeviceOps>(p.sync, a, p.spin_limit);
+            s_ok = huff_barrier::wait<huff_barrier::DeviceOps>(p.sync, a, p.spin_limit);
         __syncthreads();
-        if (!s_ok) {                       // uniform
-            if (l == 0)
-                atomicOr(p.status, PIC_HUFF_ERR_SYNC);
-            return;
-        }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (s_ok && l < 64)
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __syncthreads();
     }
-    if (!valid)
-        return;   // uniform
-    const WriteRecs r = load_write_recs(p, blk);
-    build_sorted(p, s_tab, s_u.vals, len0, val0);
-    write_phase(p, s_tab, s_words, s_u.vals, s_wsum, blk, r);
+    const bool go = a.last || s_ok;        // uniform: false for a waiter that gave up
+    if (go && valid) {
+        const WriteRecs r = load_write_recs(p, blk);
+        build_sorted(p, s_tab, s_u.vals, len0, val0);
+        write_phase(p, s_tab, s_words, s_u.vals, s_wsum, blk, r);
+    }
+    // leave (huff_barrier.h): the last to leave reports a give-up; the first
+    // workgroup's clear of the status came before its arrival, so before this
+    __syncthreads();
+    if (l == 0) {
+        uint32_t all = 0;
+        if (huff_barrier::leave<huff_barrier::DeviceOps>(p.sync + 1, (uint32_t)p.nblk,
+                                                         go ? 0u : (uint32_t)PIC_HUFF_ERR_SYNC, &all) && all)
+            atomicOr(p.status, (int32_t)all);
+    }
 }
 
 }  // namespace

@@ -76,7 +76,7 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
     h->o_flags = o;  o += align256(sizeof(int32_t) * 4);
     h->o_blk = o;    o += align256(sizeof(int32_t) * nblk);
     h->o_bnd = o;    o += align256(sizeof(int32_t) * nblk);
-    h->o_sync = o;   o += align256(sizeof(uint64_t));
+    h->o_sync = o;   o += align256(2 * sizeof(uint64_t));   // hand-off and leave words
     h->scratch_bytes = (int64_t)o;
     void *mem = nullptr;
     if (hipMalloc(&mem, o) != hipSuccess) {
@@ -87,7 +87,7 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
     h->d_scratch = static_cast<char *>(mem);
     // the one-launch path's hand-off word starts at zero; each launch leaves
     // it ready for the next
-    if (hipMemset(h->d_scratch + h->o_sync, 0, sizeof(uint64_t)) != hipSuccess ||
+    if (hipMemset(h->d_scratch + h->o_sync, 0, 2 * sizeof(uint64_t)) != hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         (void)hipGetLastError();
         (void)hipFree(mem);

@@ -162,8 +162,9 @@ struct HuffParams {
                                     // moved; bit 1: the workgroup left subsequences to the fix kernel
     int32_t nblk;                   // workgroups of the parse and write kernels
     int32_t blk_is_prefix;
-    uint64_t *sync;                 // [1]: the one-launch path's hand-off word (generation << 32 |
-                                    // arrivals), zero at create
+    uint64_t *sync;                 // [2]: the one-launch path's hand-off word (generation << 32 |
+                                    // arrivals) and leave word (error bits << 32 | departures), zero
+                                    // at create
     uint32_t spin_limit;            // polls a workgroup waits for the repair step at most
 };
 

@@ -17,6 +17,7 @@ static thread_local unsigned long long polls = 0;
 
 struct HostOps {
     static uint64_t fetch_add(uint64_t *w, uint64_t v) { return __atomic_fetch_add(w, v, __ATOMIC_SEQ_CST); }
+    static void fetch_or(uint64_t *w, uint64_t v) { (void)__atomic_fetch_or(w, v, __ATOMIC_SEQ_CST); }
     static uint64_t load(const uint64_t *w) { return __atomic_load_n(w, __ATOMIC_SEQ_CST); }
     static void store(uint64_t *w, uint64_t v) { __atomic_store_n(w, v, __ATOMIC_SEQ_CST); }
     static void pause()
@@ -131,6 +132,35 @@ int main()
         CHECK(o.gave_up == 7 && o.released == 0, "gave up %d released %d", o.gave_up, o.released);
         CHECK(o.max_polls == lim, "polls %llu", o.max_polls);
         std::printf("bound: 7 waiters gave up after %llu polls each (limit %u)\n", o.max_polls, lim);
+    }
+    // 5. leaving: every workgroup once, some with error bits; exactly one
+    //    last, which gets every bit, and the word is zero again; repeated
+    {
+        uint64_t leave_word = 0;
+        for (int g = 0; g < 100; ++g) {
+            const int n = 1 + g % 64;
+            std::atomic<int> lasts{0};
+            std::atomic<uint32_t> got{0};
+            uint32_t want = 0;
+            std::vector<std::thread> ts;
+            for (int i = 0; i < n; ++i) {
+                const uint32_t err = (i % 7 == 3) ? (1u << (i % 4)) : 0u;
+                want |= err;
+                ts.emplace_back([&, err] {
+                    uint32_t all = 0;
+                    if (hb::leave<HostOps>(&leave_word, (uint32_t)n, err, &all)) {
+                        ++lasts;
+                        got = all;
+                    }
+                });
+            }
+            for (auto &t : ts)
+                t.join();
+            CHECK(lasts == 1, "launch %d: %d last leavers", g, lasts.load());
+            CHECK(got == want, "launch %d: bits %x, want %x", g, got.load(), want);
+            CHECK(leave_word == 0, "launch %d: word %llx", g, (unsigned long long)leave_word);
+        }
+        std::printf("leave: 100 launches of 1..64 workgroups, one last leaver each with every error bit\n");
     }
     std::printf("OK\n");
     return 0;
