@@ -29,11 +29,18 @@ constexpr int TW = 16 * TWG;   // tile columns
 // starting at floor(src(o0)).  Indices past the grid are staged as the grid's
 // last sample, which is exactly the edge replication of the upsample, so every
 // pixel's second tap is at +1 (column) and +pitch (row).
+// THT: tile rows (TH, or 16 for the kernels that take taller tiles).
 __host__ __device__ constexpr int box_dim(int n, int k) { return ((n - 1 + (1 << k) - 1) >> k) + 3; }
-__host__ __device__ constexpr int box_rows(int k) { return box_dim(TH, k); }
 __host__ __device__ constexpr int box_pitch(int k) { return box_dim(TW, k); }
-__host__ __device__ constexpr int box_floats(int k) { return box_rows(k) * box_pitch(k); }
-__host__ __device__ constexpr int box_offset(int k) { return k == 0 ? 0 : box_offset(k - 1) + box_floats(k - 1); }
+template <int THT = TH>
+__host__ __device__ constexpr int box_rows(int k) { return box_dim(THT, k); }
+template <int THT = TH>
+__host__ __device__ constexpr int box_floats(int k) { return box_rows<THT>(k) * box_pitch(k); }
+template <int THT = TH>
+__host__ __device__ constexpr int box_offset(int k)
+{
+    return k == 0 ? 0 : box_offset<THT>(k - 1) + box_floats<THT>(k - 1);
+}
 
 __device__ __forceinline__ float pow2_neg(int k) { return __int_as_float((127 - k) << 23); }
 
@@ -199,7 +206,7 @@ __device__ __forceinline__ float row_sum3(float o0, float o1, float o2)
 
 // Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
 // (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
-template <int KMAX>
+template <int KMAX, int THT = TH>
 __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, int b, int ty0, int tx0, int tid)
 {
 #pragma unroll
@@ -209,8 +216,8 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
             const int hk = p.hk[k], wk = p.wk[k];
             const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
             const float *src = p.lat[k] + (int64_t)b * hk * wk;
-            float *dst = lat + box_offset(k);
-            const int n = box_floats(k), pc = box_pitch(k);   // constants once unrolled
+            float *dst = lat + box_offset<THT>(k);
+            const int n = box_floats<THT>(k), pc = box_pitch(k);   // constants once unrolled
 #pragma unroll
             for (int i0 = 0; i0 < n; i0 += kThreads) {
                 const int i = i0 + tid;
@@ -226,15 +233,16 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
 // The same staging split into a load phase (into registers) and a store
 // phase, so the loads can be in flight while other prologue work waits on
 // memory.  box_regs<KMAX>() registers per thread.
+template <int THT>
 __host__ __device__ constexpr int box_regs_from(int k, int kmax)
 {
-    return k >= kmax ? 0 : (box_floats(k) + kThreads - 1) / kThreads + box_regs_from(k + 1, kmax);
+    return k >= kmax ? 0 : (box_floats<THT>(k) + kThreads - 1) / kThreads + box_regs_from<THT>(k + 1, kmax);
 }
-template <int KMAX>
-__host__ __device__ constexpr int box_regs() { return box_regs_from(0, KMAX); }
+template <int KMAX, int THT = TH>
+__host__ __device__ constexpr int box_regs() { return box_regs_from<THT>(0, KMAX); }
 
-template <int KMAX>
-__device__ __forceinline__ void load_boxes(float (&v)[box_regs<KMAX>()], const DecodeParams &p, int b, int ty0,
+template <int KMAX, int THT = TH>
+__device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], const DecodeParams &p, int b, int ty0,
                                            int tx0, int tid)
 {
     int idx = 0;
@@ -245,7 +253,7 @@ __device__ __forceinline__ void load_boxes(float (&v)[box_regs<KMAX>()], const D
         const int hk = p.hk[k], wk = p.wk[k];
         const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
         const float *src = p.lat[k] + (int64_t)b * hk * wk;
-        const int n = box_floats(k), pc = box_pitch(k);
+        const int n = box_floats<THT>(k), pc = box_pitch(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {
             const int i = min(i0 + tid, n - 1);
@@ -255,19 +263,19 @@ __device__ __forceinline__ void load_boxes(float (&v)[box_regs<KMAX>()], const D
     }
 }
 
-template <int KMAX>
-__device__ __forceinline__ void store_boxes(float *lat, const float (&v)[box_regs<KMAX>()], const DecodeParams &p,
+template <int KMAX, int THT = TH>
+__device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_regs<KMAX, THT>())], const DecodeParams &p,
                                             int tid)
 {
     int idx = 0;
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
-        const int n = box_floats(k);
+        const int n = box_floats<THT>(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {
             const int i = i0 + tid;
             if (k < p.L && i < n)
-                lat[box_offset(k) + i] = v[idx];
+                lat[box_offset<THT>(k) + i] = v[idx];
             ++idx;
         }
     }
@@ -285,10 +293,11 @@ struct LaneLevel {
     float clx[TWG];   // horizontal lerp weight, per column group
 };
 
+template <int THT = TH>
 __device__ __forceinline__ void lane_level_init(LaneLevel &lv, int k, int lat_base)
 {
     lv.inv = pow2_neg(k);
-    lv.loff = lat_base + box_offset(k);
+    lv.loff = lat_base + box_offset<THT>(k);
     lv.pitch = box_pitch(k);
 }
 

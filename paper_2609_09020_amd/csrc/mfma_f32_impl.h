@@ -63,7 +63,7 @@ using namespace tile;
 // of every address is uniform and the column part is the lane's own.
 __host__ __device__ constexpr int swz(int n) { return (n & ~15) | ((n & 3) << 2) | ((n >> 2) & 3); }
 
-template <int NB, int NH, int LS, int KSH>
+template <int NB, int NH, int LS, int KSH, int THT>
 struct Layout {
     static constexpr int N = 16 * NB;                               // padded hidden width
     static constexpr int KSH4 = (KSH + 3) / 4;                      // quads of hidden K steps
@@ -75,7 +75,7 @@ struct Layout {
     static constexpr int BIAS = WH + NH * N * PITCH;                // [NH + 1][N]
     static constexpr int W3 = BIAS + (NH + 1) * N;                  // [3][N]
     static constexpr int LAT = W3 + 3 * N;                          // latent boxes
-    static constexpr int SIZE = LAT + box_offset(4 * LS);
+    static constexpr int SIZE = LAT + box_offset<THT>(4 * LS);
 };
 
 // Neuron on row `row` of an output block; the map is its own inverse.
@@ -83,12 +83,14 @@ __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: K steps of
 // the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
-// 4 KSH and up are padding and skipped).
-template <int NB, int NH, int LS, int KSH>
+// 4 KSH and up are padding and skipped); RPW: tile rows per wavefront (a tile
+// is 4 RPW rows: 8, or 16 when the launch has tiles to spare).
+template <int NB, int NH, int LS, int KSH, int RPW>
 __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
-    using LY = Layout<NB, NH, LS, KSH>;
+    constexpr int THT = kWaves * RPW;   // tile rows
+    using LY = Layout<NB, NH, LS, KSH, THT>;
     constexpr int N = LY::N, PITCH = LY::PITCH;
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
 
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
     const float *b3 = layer_params(p, NH + 1, b).b;
     const float b3_0 = b3[0], b3_1 = b3[1], b3_2 = b3[2];
 
-    float boxv[box_regs<4 * LS>()];
+    float boxv[box_regs<4 * LS, THT>()];
     float w1[NB][LS];
 
     // ---- parameters.  Every load is issued before the first is waited for:
@@ -179,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         // the first tile's latent loads go out behind the parameters: loads
         // complete in order, so the stores below need not wait for them
         if (blk < tiles)
-            load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
+            load_boxes<4 * LS, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
         // zero what lies outside each layer's shape
         const int r1 = row_neuron(col);
 #pragma unroll
@@ -207,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         }
     }
     if (blk < tiles)
-        store_boxes<4 * LS>(lds + LY::LAT, boxv, p, tid);
+        store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
     // ---- the level each lane samples for K step s of the first layer.  Lanes
@@ -217,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
 #pragma unroll
     for (int s = 0; s < LS; ++s) {
         const int k = 4 * s + g;
-        lane_level_init(lv[s], k < L ? k : 0, LY::LAT);
+        lane_level_init<THT>(lv[s], k < L ? k : 0, LY::LAT);
     }
 
     const int H = p.H, W = p.W;
@@ -239,12 +241,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
-        const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
+        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
             __syncthreads();   // every wavefront is done with the previous tile's boxes
-            stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
+            stage_boxes<4 * LS, THT>(lds + LY::LAT, p, b, ty0, tx0, tid);
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
@@ -259,8 +261,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int block
         // instead of oldest first, and none is left to run alone at the end.
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll 1
-        for (int rr = 0; rr < 2; ++rr) {
-            const int y = ty0 + 2 * wave + rr;
+        for (int rr = 0; rr < RPW; ++rr) {
+            const int y = ty0 + RPW * wave + rr;
             if (y > ty1)
                 break;   // wave-uniform: the row lies below the image
 
@@ -378,19 +380,34 @@ int hidden_blocks(int nl, const int32_t *widths);
 // the output layer's sums, so the last hidden width counts as well.
 int hidden_ksteps(int nl, const int32_t *widths);
 
-template <int NB, int NH, int LS, int KSH>
-hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+template <int NB, int NH, int LS, int KSH, int RPW>
+hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int tiles, int bpi)
 {
-    const int tiles_x = (p.W + TW - 1) / TW, tiles_y = (p.H + TH - 1) / TH;
-    const int tiles = tiles_x * tiles_y;
-    static int occ = 0;
-    const int bpi = blocks_per_image(k_mfma_f32<NB, NH, LS, KSH>, p, num_cus, tiles, occ);
     const int64_t nblocks = (int64_t)bpi * p.batch;
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_mfma_f32<NB, NH, LS, KSH>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
+    hipLaunchKernelGGL((k_mfma_f32<NB, NH, LS, KSH, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
                        tiles_x, tiles);
     return hipGetLastError();
+}
+
+// 16-row tiles (4 rows per wavefront) when every workgroup of the launch
+// averages two or more of them and the taller boxes cost no occupancy: the
+// per-tile work (box staging, its two barriers, the tile's level geometry)
+// then spreads over twice the pixels.  Else 8-row tiles, so that a single
+// small image still fills the device.
+template <int NB, int NH, int LS, int KSH>
+hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+{
+    const int tiles_x = (p.W + TW - 1) / TW;
+    const int tiles8 = tiles_x * ((p.H + TH - 1) / TH);
+    const int tiles16 = tiles_x * ((p.H + 4 * kWaves - 1) / (4 * kWaves));
+    static int occ8 = 0, occ16 = 0;   // workgroups per CU of each instance
+    const int bpi8 = blocks_per_image(k_mfma_f32<NB, NH, LS, KSH, 2>, p, num_cus, tiles8, occ8);
+    const int bpi16 = blocks_per_image(k_mfma_f32<NB, NH, LS, KSH, 4>, p, num_cus, tiles16, occ16);
+    if (occ16 >= occ8 && tiles16 >= 2 * bpi16)
+        return launch_rows<NB, NH, LS, KSH, 4>(p, s, tiles_x, tiles16, bpi16);
+    return launch_rows<NB, NH, LS, KSH, 2>(p, s, tiles_x, tiles8, bpi8);
 }
 
 template <int NH>

@@ -254,6 +254,18 @@ def test_reference_family_matches_binary32_model(case):
     assert n == 0, f"{n} values differ from the binary32 model"
 
 
+# Batches large enough for the fp32 matrix-core family's 16-row tiles (it
+# takes them when every workgroup averages two or more: with 64 images,
+# 16 workgroups per image at 4 per CU, and an image of 200 x 300 has
+# 5 x 13 = 65 such tiles), at sizes ragged against both tile dimensions
+# (200 = 12 x 16 + 8 rows, 300 = 4 x 64 + 44 columns), raw outputs.
+@pytest.mark.parametrize("case", [(200, 300, (7, 40, 40, 3), 64, 31, False),
+                                  (200, 300, (4, 16, 16, 3), 64, 32, True),
+                                  (136, 330, (8, 48, 48, 3), 64, 33, False)], ids=str)
+def test_tall_tiles_ragged_batch(case):
+    _run_case(case, "mfma_f32")
+
+
 def test_shared_weights_stride_zero_matches_repeated():
     inp = synth.make_inputs(37, 53, 6, (6, 24, 24, 3), batch=3, seed=5, latent="normal",
                             bias="normal", shared_weights=True)
