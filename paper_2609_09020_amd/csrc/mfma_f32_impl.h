@@ -84,9 +84,13 @@ __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: K steps of
 // the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
 // 4 KSH and up are padding and skipped); RPW: tile rows per wavefront (a tile
-// is 4 RPW rows: 8, or 16 when the launch has tiles to spare).
+// is 4 RPW rows: 8, or 16 when the launch has tiles to spare).  The 64-wide
+// 16-row instances are held to 128 VGPRs (4 wavefronts per SIMD, as their
+// 8-row ones; unconstrained they take 145); held there, the 40- and 48-wide
+// ones measured slower at the same register count, so they are not.
 template <int NB, int NH, int LS, int KSH, int RPW>
-__global__ __launch_bounds__(kThreads) void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(RPW == 4 && NB == 4 && LS <= 2 ? 4 : 1)))
+void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
     constexpr int THT = kWaves * RPW;   // tile rows
