@@ -39,7 +39,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-template <int NB, int NH, int LPG>
+template <int NB, int NH, int LPG, int THT>
 struct Layout {
     static constexpr int KS2 = (NB + 1) / 2;                        // hidden K steps (32 inputs each)
     static constexpr int W1A = 0;                                   // u32 [NB][64][4]
@@ -48,7 +48,7 @@ struct Layout {
     static constexpr int BH = B1 + NB * 64 * 4;                     // f32 [NH][NB][64][4]
     static constexpr int W3 = BH + NH * NB * 64 * 4;                // f32 [NB][4 r][4 g][4 c]
     static constexpr int LAT = W3 + NB * 64;                        // latent boxes
-    static constexpr int SIZE = LAT + box_offset(4 * LPG);
+    static constexpr int SIZE = LAT + box_offset<THT>(4 * LPG);
 };
 
 // (x0, x1) -> {hi, lo}: the packed bfloat16 pairs (hi0, hi1) and (lo0, lo1),
@@ -89,12 +89,15 @@ __host__ __device__ constexpr int l1_level(int w, int h)
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LPG: levels
-// per lane group in the first layer (ceil(L / 4)).
-template <int NB, int NH, int LPG>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <= 2 ? 4 : 1))) void k_mfma_bf16(DecodeParams p, int blocks_per_image,
-                                                        int tiles_x, int tiles)
+// per lane group in the first layer (ceil(L / 4)); RPW: tile rows per
+// wavefront (a tile is 4 RPW rows: 8, or 16 when the launch has tiles to
+// spare).
+template <int NB, int NH, int LPG, int RPW>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <= 2 ? 4 : 1)))
+void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
 {
-    using LY = Layout<NB, NH, LPG>;
+    constexpr int THT = kWaves * RPW;   // tile rows
+    using LY = Layout<NB, NH, LPG, THT>;
     constexpr int KS2 = LY::KS2;
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
     unsigned *ldsu = reinterpret_cast<unsigned *>(lds);
@@ -116,9 +119,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
 
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
-    float boxv[box_regs<4 * LPG>()];
+    float boxv[box_regs<4 * LPG, THT>()];
     if (blk < tiles)
-        load_boxes<4 * LPG>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
+        load_boxes<4 * LPG, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
 
     // ---- stage this image's parameters into LDS in operand layouts (every
     // load in flight before the first store)
@@ -185,7 +188,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
         store_part(lds + LY::W3, w3);
     }
     if (blk < tiles)
-        store_boxes<4 * LPG>(lds + LY::LAT, boxv, p, tid);
+        store_boxes<4 * LPG, THT>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
 
@@ -195,7 +198,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
 #pragma unroll
     for (int j = 0; j < LPG; ++j) {
         const int k = LPG * g + j;
-        lane_level_init(lv[j], k < L ? k : 0, LY::LAT);
+        lane_level_init<THT>(lv[j], k < L ? k : 0, LY::LAT);
     }
 
     const int H = p.H, W = p.W;
@@ -213,12 +216,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
-        const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
+        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
             __syncthreads();   // every wavefront is done with the previous tile's boxes
-            stage_boxes<4 * LPG>(lds + LY::LAT, p, b, ty0, tx0, tid);
+            stage_boxes<4 * LPG, THT>(lds + LY::LAT, p, b, ty0, tx0, tid);
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
@@ -229,8 +232,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
             lane_level_tile(lv[j], ty0, tx0, tx1, col);
 
 #pragma unroll 1
-        for (int rr = 0; rr < 2; ++rr) {
-            const int y = ty0 + 2 * wave + rr;
+        for (int rr = 0; rr < RPW; ++rr) {
+            const int y = ty0 + RPW * wave + rr;
             if (y > ty1)
                 break;
             int roff[LPG];
@@ -361,19 +364,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <=
     }
 }
 
-template <int NB, int NH, int LPG>
-hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+template <int NB, int NH, int LPG, int RPW>
+hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int tiles, int bpi)
 {
-    const int tiles_x = (p.W + TW - 1) / TW, tiles_y = (p.H + TH - 1) / TH;
-    const int tiles = tiles_x * tiles_y;
-    static int occ = 0;
-    const int bpi = blocks_per_image(k_mfma_bf16<NB, NH, LPG>, p, num_cus, tiles, occ);
     const int64_t nblocks = (int64_t)bpi * p.batch;
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_mfma_bf16<NB, NH, LPG>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
+    hipLaunchKernelGGL((k_mfma_bf16<NB, NH, LPG, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
                        tiles_x, tiles);
     return hipGetLastError();
+}
+
+// 16-row tiles when every workgroup of the launch averages two or more and
+// the taller boxes cost no occupancy (as in the fp32 family), else 8-row.
+template <int NB, int NH, int LPG>
+hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+{
+    const int tiles_x = (p.W + TW - 1) / TW;
+    const int tiles8 = tiles_x * ((p.H + TH - 1) / TH);
+    const int tiles16 = tiles_x * ((p.H + 4 * kWaves - 1) / (4 * kWaves));
+    static int occ8 = 0, occ16 = 0;   // workgroups per CU of each instance
+    const int bpi8 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 2>, p, num_cus, tiles8, occ8);
+    const int bpi16 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 4>, p, num_cus, tiles16, occ16);
+    if (occ16 >= occ8 && tiles16 >= 2 * bpi16)
+        return launch_rows<NB, NH, LPG, 4>(p, s, tiles_x, tiles16, bpi16);
+    return launch_rows<NB, NH, LPG, 2>(p, s, tiles_x, tiles8, bpi8);
 }
 
 int hidden_blocks(int nl, const int32_t *widths);

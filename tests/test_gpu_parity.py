@@ -266,6 +266,13 @@ def test_tall_tiles_ragged_batch(case):
     _run_case(case, "mfma_f32")
 
 
+# The bf16 family's 16-row tiles (same rule), ragged likewise.
+@pytest.mark.parametrize("case", [(200, 300, (8, 64, 64, 3), 64, 34, False),
+                                  (136, 330, (7, 40, 40, 3), 64, 35, True)], ids=str)
+def test_tall_tiles_ragged_batch_bf16(case):
+    test_fuzz_bf16_weights(case, "mfma_bf16")
+
+
 def test_shared_weights_stride_zero_matches_repeated():
     inp = synth.make_inputs(37, 53, 6, (6, 24, 24, 3), batch=3, seed=5, latent="normal",
                             bias="normal", shared_weights=True)
