@@ -55,7 +55,7 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 // ceil(Q / 2) (hi, hi) pairs, four pairs a step.
 __host__ __device__ constexpr int ksteps(int q) { return (q + (q + 1) / 2 + 3) / 4; }
 
-template <int NB, int NH, int LS, int KSH>
+template <int NB, int NH, int LS, int KSH, int THT>
 struct Layout {
     static constexpr int S1 = ksteps(LS);                           // first-layer K steps
     static constexpr int SH = ksteps(KSH);                          // hidden-layer K steps
@@ -66,7 +66,7 @@ struct Layout {
     static constexpr int W3 = BH + NH * NB * 256;                   // f32 [NB][4 r][4 g][4 c]
     static constexpr int WSC = W3 + NB * 64;                        // f32 [NH + 1][kWaves]: weight maxima
     static constexpr int LAT = WSC + (NH + 1) * kWaves;             // latent boxes
-    static constexpr int SIZE = LAT + box_offset(4 * LS);
+    static constexpr int SIZE = LAT + box_offset<THT>(4 * LS);
     // the parameters as the caller lays them out are first staged in the
     // regions their operand layouts then replace (each is large enough)
     static constexpr int N = 16 * NB;
@@ -207,13 +207,15 @@ __device__ __forceinline__ float wave_max(float x)
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: levels per
 // lane group (ceil(L / 4)); KSH: values per lane group of the hidden layers'
-// inputs (ceil(width / 4)).
-template <int NB, int NH, int LS, int KSH>
+// inputs (ceil(width / 4)); RPW: tile rows per wavefront (a tile is 4 RPW
+// rows: 8, or 16 when the launch has tiles to spare).
+template <int NB, int NH, int LS, int KSH, int RPW>
 __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blocks_per_image, int tiles_x,
                                                          int tiles)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
-    using LY = Layout<NB, NH, LS, KSH>;
+    constexpr int THT = kWaves * RPW;   // tile rows
+    using LY = Layout<NB, NH, LS, KSH, THT>;
     constexpr int S1 = LY::S1, SH = LY::SH;
     __shared__ __attribute__((aligned(16))) float lds[LY::SIZE];
     unsigned *ldsu = reinterpret_cast<unsigned *>(lds);
@@ -235,9 +237,9 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
 
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
-    float boxv[box_regs<4 * LS>()];
+    float boxv[box_regs<4 * LS, THT>()];
     if (blk < tiles)
-        load_boxes<4 * LS>(boxv, p, b, (blk / tiles_x) * TH, (blk % tiles_x) * TW, tid);
+        load_boxes<4 * LS, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
 
     // ---- this image's parameters: contiguous loads (all in flight at once)
     // into LDS as the caller lays them out, then scaled, split into fp16
@@ -339,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
         store_part(lds + LY::W3, w3);
     }
     if (blk < tiles)
-        store_boxes<4 * LS>(lds + LY::LAT, boxv, p, tid);
+        store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
     // ---- the level each lane samples as its value q of the first layer:
@@ -348,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
 #pragma unroll
     for (int s = 0; s < LS; ++s) {
         const int k = 4 * s + g;
-        lane_level_init(lv[s], k < L ? k : 0, LY::LAT);
+        lane_level_init<THT>(lv[s], k < L ? k : 0, LY::LAT);
     }
 
     const int H = p.H, W = p.W;
@@ -368,12 +370,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * TH, tx0 = (t % tiles_x) * TW;
-        const int ty1 = min(ty0 + TH, H) - 1, tx1 = min(tx0 + TW, W) - 1;
+        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
             __syncthreads();   // every wavefront is done with the previous tile's boxes
-            stage_boxes<4 * LS>(lds + LY::LAT, p, b, ty0, tx0, tid);
+            stage_boxes<4 * LS, THT>(lds + LY::LAT, p, b, ty0, tx0, tid);
             __syncthreads();
         }
         int ticket = 0;    // the tile after this one; its latency hides behind the tile
@@ -384,8 +386,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
             lane_level_tile(lv[s], ty0, tx0, tx1, col);
 
 #pragma unroll 1
-        for (int rr = 0; rr < 2; ++rr) {
-            const int y = ty0 + 2 * wave + rr;
+        for (int rr = 0; rr < RPW; ++rr) {
+            const int y = ty0 + RPW * wave + rr;
             if (y > ty1)
                 break;   // wave-uniform: the row lies below the image
             int roff[LS];
@@ -502,19 +504,31 @@ int hidden_blocks(int nl, const int32_t *widths);
 // widest hidden layer (the last one feeds the output layer, so it counts too).
 int hidden_values(int nl, const int32_t *widths);
 
-template <int NB, int NH, int LS, int KSH>
-hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+template <int NB, int NH, int LS, int KSH, int RPW>
+hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int tiles, int bpi)
 {
-    const int tiles_x = (p.W + TW - 1) / TW, tiles_y = (p.H + TH - 1) / TH;
-    const int tiles = tiles_x * tiles_y;
-    static int occ = 0;
-    const int bpi = blocks_per_image(k_mfma_f16x3<NB, NH, LS, KSH>, p, num_cus, tiles, occ);
     const int64_t nblocks = (int64_t)bpi * p.batch;
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_mfma_f16x3<NB, NH, LS, KSH>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
-                       tiles_x, tiles);
+    hipLaunchKernelGGL((k_mfma_f16x3<NB, NH, LS, KSH, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p,
+                       bpi, tiles_x, tiles);
     return hipGetLastError();
+}
+
+// 16-row tiles when every workgroup of the launch averages two or more and
+// the taller boxes cost no occupancy (as in the fp32 family), else 8-row.
+template <int NB, int NH, int LS, int KSH>
+hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
+{
+    const int tiles_x = (p.W + TW - 1) / TW;
+    const int tiles8 = tiles_x * ((p.H + TH - 1) / TH);
+    const int tiles16 = tiles_x * ((p.H + 4 * kWaves - 1) / (4 * kWaves));
+    static int occ8 = 0, occ16 = 0;   // workgroups per CU of each instance
+    const int bpi8 = blocks_per_image(k_mfma_f16x3<NB, NH, LS, KSH, 2>, p, num_cus, tiles8, occ8);
+    const int bpi16 = blocks_per_image(k_mfma_f16x3<NB, NH, LS, KSH, 4>, p, num_cus, tiles16, occ16);
+    if (occ16 >= occ8 && tiles16 >= 2 * bpi16)
+        return launch_rows<NB, NH, LS, KSH, 4>(p, s, tiles_x, tiles16, bpi16);
+    return launch_rows<NB, NH, LS, KSH, 2>(p, s, tiles_x, tiles8, bpi8);
 }
 
 template <int NH>
