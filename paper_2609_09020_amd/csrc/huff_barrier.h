@@ -14,7 +14,7 @@
 //
 // The last arrival can only come once every workgroup has started: a waiter
 // that holds a CU while others of the launch wait for one could wait for
-// ever, so a waiter stops after `spin_limit` polls and reports it.
+// ever, so a waiter stops after a time limit and reports it.
 //
 // Leaving: a second word, error bits << 32 | departures, also zero at
 // create.  Every workgroup leaves once, after its last write, whatever path
@@ -32,6 +32,7 @@
 //   uint64_t Ops::load(const uint64_t *w)
 //   void     Ops::store(uint64_t *w, uint64_t v)
 //   void     Ops::pause()                               between polls
+//   uint64_t Ops::now()                                 a clock the wait's limit is in
 #pragma once
 
 #include <stdint.h>
@@ -69,12 +70,13 @@ PIC_HD inline void release(uint64_t *word, const Arrival &a)
     Ops::store(word, (uint64_t)(a.generation + 1u) << 32);
 }
 
-// A waiter: poll until the generation it arrived in has ended, at most
-// `spin_limit` times.  True when released, false when it gave up.
+// A waiter: poll until the generation it arrived in has ended, for at most
+// `limit` units of Ops::now().  True when released, false when it gave up.
 template <class Ops>
-PIC_HD inline bool wait(const uint64_t *word, const Arrival &a, uint32_t spin_limit)
+PIC_HD inline bool wait(const uint64_t *word, const Arrival &a, uint64_t limit)
 {
-    for (uint32_t i = 0; i < spin_limit; ++i) {
+    const uint64_t t0 = Ops::now();
+    while (Ops::now() - t0 < limit) {
         if ((uint32_t)(Ops::load(word) >> 32) != a.generation)
             return true;
         Ops::pause();
@@ -100,7 +102,8 @@ PIC_HD inline bool leave(uint64_t *word, uint32_t n, uint32_t err, uint32_t *all
 
 #if defined(__HIPCC__)
 // The kernels' policy: device-scope atomics on the scratch words (one
-// coherent place for every XCD), a short sleep between polls.
+// coherent place for every XCD), a short sleep between polls, the wait's
+// limit in ticks of the 100 MHz real-time counter.
 struct DeviceOps {
     __device__ static uint64_t fetch_add(uint64_t *w, uint64_t v)
     {
@@ -119,6 +122,7 @@ struct DeviceOps {
         __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __device__ static void pause() { __builtin_amdgcn_s_sleep(2); }
+    __device__ static uint64_t now() { return __builtin_amdgcn_s_memrealtime(); }
 };
 #endif
 

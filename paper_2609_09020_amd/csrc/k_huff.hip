@@ -874,7 +874,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_write(HuffParams p)
 // workgroups.  Each workgroup builds the tables and stages its words once,
 // parses, and arrives at the hand-off (huff_barrier.h); the last to arrive
 // runs the repair step, then releases the others, which wait at most
-// p.spin_limit polls (a workgroup that gives up sets PIC_HUFF_ERR_SYNC and
+// p.wait_ticks of the real-time counter (a workgroup that gives up sets PIC_HUFF_ERR_SYNC and
 // writes nothing).  At most 64 workgroups of 36 KB of LDS (four fit on one
 // CU) are resident together on an otherwise idle device; only another
 // kernel that holds the CUs past the wait bound makes a waiter give up, and
@@ -950,7 +950,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
             huff_barrier::release<huff_barrier::DeviceOps>(p.sync, a);
     } else {
         if (l == 0)
-            s_ok = huff_barrier::wait<huff_barrier::DeviceOps>(p.sync, a, p.spin_limit);
+            s_ok = huff_barrier::wait<huff_barrier::DeviceOps>(p.sync, a, p.wait_ticks);
         __syncthreads();
         if (s_ok && l < 64)
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");

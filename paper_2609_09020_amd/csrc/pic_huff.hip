@@ -140,7 +140,7 @@ pic_status pic_huff_decode(pic_huff *h, const uint8_t *data, int64_t n_bits, con
     p.nblk = (p.nsub + pic::kHuffOwn - 1) / pic::kHuffOwn;
     p.blk_is_prefix = p.nblk > pic::kHuffPrefixInKernelMax;
     p.sync = reinterpret_cast<uint64_t *>(h->d_scratch + h->o_sync);
-    p.spin_limit = pic::kHuffSpinLimit;
+    p.wait_ticks = pic::kHuffWaitTicks;
     if (pic::launch_huff(p, (hipStream_t)stream) != hipSuccess) {
         (void)hipGetLastError();
         return PIC_E_HIP;

@@ -134,7 +134,7 @@ constexpr int kHuffLutBits = 11;               // first-level decode table: 2^11
 constexpr int kHuffMaxLen = 24;
 constexpr int kHuffMaxTable = 4096;
 constexpr int kHuffOneLaunchMax = 64;          // workgroups: one launch (parse, repair, write)
-constexpr uint32_t kHuffSpinLimit = 1u << 22;  // polls of 128 cycles: about 0.2 s
+constexpr uint64_t kHuffWaitTicks = 20000000;  // a waiter's limit: 0.2 s of the 100 MHz real-time counter
 
 // Kernel argument of the entropy-decoding kernels.
 struct HuffParams {
@@ -165,7 +165,7 @@ struct HuffParams {
     uint64_t *sync;                 // [2]: the one-launch path's hand-off word (generation << 32 |
                                     // arrivals) and leave word (error bits << 32 | departures), zero
                                     // at create
-    uint32_t spin_limit;            // polls a workgroup waits for the repair step at most
+    uint64_t wait_ticks;            // how long a workgroup waits for the repair step at most (100 MHz ticks)
 };
 
 hipError_t launch_huff(const HuffParams &p, hipStream_t s);

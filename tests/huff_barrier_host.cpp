@@ -25,6 +25,8 @@ struct HostOps {
         ++polls;
         std::this_thread::yield();
     }
+    // the wait's limit counted in polls here
+    static uint64_t now() { return polls; }
 };
 
 #define CHECK(c, ...)                                                   \
