@@ -90,8 +90,8 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LPG: levels
 // per lane group in the first layer (ceil(L / 4)); RPW: tile rows per
-// wavefront (a tile is 4 RPW rows: 8, or 16 when the launch has tiles to
-// spare).
+// wavefront (a tile is 4 RPW rows: 8, or 16 or 32 when the launch has tiles
+// to spare).
 template <int NB, int NH, int LPG, int RPW>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <= 2 ? 4 : 1)))
 void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
@@ -375,8 +375,9 @@ hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int ti
     return hipGetLastError();
 }
 
-// 16-row tiles when every workgroup of the launch averages two or more and
-// the taller boxes cost no occupancy (as in the fp32 family), else 8-row.
+// 32- or 16-row tiles when every workgroup of the launch averages two or
+// more of them and the taller boxes cost no occupancy (as in the fp32
+// family), else 8-row.
 template <int NB, int NH, int LPG>
 hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
 {
@@ -386,6 +387,11 @@ hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
     static int occ8 = 0, occ16 = 0;   // workgroups per CU of each instance
     const int bpi8 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 2>, p, num_cus, tiles8, occ8);
     const int bpi16 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 4>, p, num_cus, tiles16, occ16);
+    const int tiles32 = tiles_x * ((p.H + 8 * kWaves - 1) / (8 * kWaves));
+    static int occ32 = 0;
+    const int bpi32 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 8>, p, num_cus, tiles32, occ32);
+    if (occ32 >= occ8 && tiles32 >= 2 * bpi32)
+        return launch_rows<NB, NH, LPG, 8>(p, s, tiles_x, tiles32, bpi32);
     if (occ16 >= occ8 && tiles16 >= 2 * bpi16)
         return launch_rows<NB, NH, LPG, 4>(p, s, tiles_x, tiles16, bpi16);
     return launch_rows<NB, NH, LPG, 2>(p, s, tiles_x, tiles8, bpi8);
