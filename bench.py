@@ -251,8 +251,9 @@ def peaks(args):
     """Peak issue rates on this GPU (microbenchmarks that ground the kernel
     design): fp32 / bf16 / fp16 matrix instructions and fp32 vector
     FMAs, each with independent accumulators, the fp32 and bf16 matrix
-    instructions interleaved with vector FMAs in the same wavefronts, and a
-    device-to-device copy.  One JSON line per measurement."""
+    instructions interleaved with vector FMAs in the same wavefronts, a
+    device-to-device copy, and what an empty kernel launch costs back to back
+    (from a host loop and from a graph).  One JSON line per measurement."""
     import ctypes
     import torch
     from paper_2609_09020_amd import build as B
@@ -311,6 +312,22 @@ def peaks(args):
     ms, _ = time_calls(lambda: dst.copy_(src), 20, 3, stream)
     print(json.dumps({"peaks": "device copy (torch copy_ of 1 GiB)", "ms": round(ms, 4),
                       "read_plus_write_gbs": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
+    del src, dst
+    # What a launch costs with nothing in it: an empty kernel, 200 launches
+    # back to back, from a host loop and replayed from a graph.
+    lib.pic_peaks_launch_cadence.restype = ctypes.c_int
+    lib.pic_peaks_launch_cadence.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                             ctypes.POINTER(ctypes.c_float)]
+    buf = torch.empty(4096, dtype=torch.float32, device=dev)
+    for blocks in (1, 256, 768, 3072):
+        rec = {"peaks": "empty kernel launch", "workgroups": blocks, "threads": 256}
+        for graph in (0, 1):
+            us = ctypes.c_float(0.0)
+            st = lib.pic_peaks_launch_cadence(blocks, 200, graph, ctypes.c_void_p(buf.data_ptr()), ctypes.byref(us))
+            if st:
+                raise RuntimeError(f"pic_peaks_launch_cadence failed: {st}")
+            rec["graph_us_per_launch" if graph else "host_loop_us_per_launch"] = round(us.value, 3)
+        print(json.dumps(rec), flush=True)
 
 
 def width_sweep(args):

@@ -16,6 +16,12 @@
 //
 // The vector FMAs are built with packed fp32 disabled, like the decoder, so
 // they are single v_fma_f32 instructions (64 lanes x 2 FLOP).
+//
+// pic_peaks_launch_cadence measures what a launch costs with no work in it:
+// an empty kernel (it reads one kernel-argument word and exits) launched n
+// times back to back, either from a host loop (the rate the host can enqueue
+// at) or replayed from a HIP graph of the same n launches (the device's own
+// cadence, no host work per launch).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -85,7 +91,71 @@ __global__ __launch_bounds__(kThreads) void k_peak(int iters, float seed, float 
     out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = s;
 }
 
+struct EmptyArgs {
+    float *out;
+    int32_t pad[100];   // a kernel argument of about the decoder's size
+};
+
+__global__ __launch_bounds__(kThreads) void k_empty(EmptyArgs a)
+{
+    if (a.pad[99] == 12345 && threadIdx.x == 0)   // never (the host zeroes pad)
+        a.out[blockIdx.x] = 1.0f;
+}
+
 }  // namespace
+
+// Average microseconds per launch of k_empty over `n` back-to-back launches
+// of `blocks` workgroups of 256 threads on a stream of its own: from a host
+// loop (use_graph 0) or replayed from a captured graph (use_graph 1).  `out`
+// is a device buffer of at least `blocks` floats, never written in practice.
+// Returns 0, or non-zero on bad arguments or a HIP error.
+extern "C" __attribute__((visibility("default")))
+int pic_peaks_launch_cadence(int blocks, int n, int use_graph, float *out, float *us_per_launch)
+{
+    if (blocks < 1 || n < 1 || !out || !us_per_launch)
+        return 1;
+    EmptyArgs a{};
+    a.out = out;
+    hipStream_t s = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipGraph_t gr = nullptr;
+    hipGraphExec_t ge = nullptr;
+    const dim3 g((unsigned)blocks), t(kThreads);
+    bool ok = hipStreamCreate(&s) == hipSuccess && hipEventCreate(&e0) == hipSuccess &&
+              hipEventCreate(&e1) == hipSuccess;
+    auto launches = [&] {
+        for (int i = 0; i < n; ++i)
+            hipLaunchKernelGGL(k_empty, g, t, 0, s, a);
+    };
+    if (ok && use_graph) {
+        ok = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) == hipSuccess;
+        if (ok) {
+            launches();
+            ok = hipStreamEndCapture(s, &gr) == hipSuccess &&
+                 hipGraphInstantiate(&ge, gr, nullptr, nullptr, 0) == hipSuccess;
+        }
+    }
+    auto run = [&] { return use_graph ? hipGraphLaunch(ge, s) == hipSuccess : (launches(), true); };
+    float ms = 0.0f;
+    ok = ok && run() && hipStreamSynchronize(s) == hipSuccess;                 // warm-up
+    ok = ok && hipEventRecord(e0, s) == hipSuccess && run() && hipEventRecord(e1, s) == hipSuccess &&
+         hipEventSynchronize(e1) == hipSuccess && hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+    ok = ok && hipGetLastError() == hipSuccess;
+    if (ge)
+        (void)hipGraphExecDestroy(ge);
+    if (gr)
+        (void)hipGraphDestroy(gr);
+    if (e0)
+        (void)hipEventDestroy(e0);
+    if (e1)
+        (void)hipEventDestroy(e1);
+    if (s)
+        (void)hipStreamDestroy(s);
+    if (!ok)
+        return 2;
+    *us_per_launch = 1e3f * ms / (float)n;
+    return 0;
+}
 
 extern "C" __attribute__((visibility("default")))
 int pic_peaks_launch(int kind, int blocks, int iters, float *out, void *stream)
