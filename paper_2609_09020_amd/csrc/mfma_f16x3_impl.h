@@ -36,8 +36,11 @@
 //     p < Q            (x_h, x_l) of v_p, against (w_h, w_h),
 //     Q <= p < Q + T   (x_h of v_2t, x_h of v_2t+1), t = p - Q, against their w_l,
 //   T = ceil(Q / 2); four pairs a K step, the rest zero.  The weights are
-//   scaled, split and laid out to match once per workgroup.  The output
-//   layer (3 neurons) runs in fp32 on the vector ALU.
+//   scaled, split and laid out to match once per workgroup, a pair of inputs
+//   of one neuron at a time (AItems below).  A layer's biases sit in LDS
+//   once per neuron, in the order that gives lane group g the four neurons
+//   16 ob + 4 r + g of its registers as one 16-byte read.  The output layer
+//   (3 neurons) runs in fp32 on the vector ALU.
 #pragma once
 
 #include "decode_common.h"
@@ -61,36 +64,16 @@ struct Layout {
     static constexpr int SH = ksteps(KSH);                          // hidden-layer K steps
     static constexpr int W1A = 0;                                   // u32 [NB][S1][64][4]
     static constexpr int WHA = W1A + NB * S1 * 256;                 // u32 [NH][NB][SH][64][4]
-    static constexpr int B1 = WHA + NH * NB * SH * 256;             // f32 [NB][64][4]
-    static constexpr int BH = B1 + NB * 256;                        // f32 [NH][NB][64][4]
-    static constexpr int W3 = BH + NH * NB * 256;                   // f32 [NB][4 r][4 g][4 c]
+    static constexpr int B1 = WHA + NH * NB * SH * 256;             // f32 [NH + 1][16 NB], swz order
+    static constexpr int W3 = B1 + (NH + 1) * 16 * NB;              // f32 [NB][4 r][4 g][4 c]
     static constexpr int WSC = W3 + NB * 64;                        // f32 [NH + 1][kWaves]: weight maxima
     static constexpr int LAT = WSC + (NH + 1) * kWaves;             // latent boxes
     static constexpr int SIZE = LAT + box_offset<THT>(4 * LS);
-    // the parameters as the caller lays them out are first staged in the
-    // regions their operand layouts then replace (each is large enough)
     static constexpr int N = 16 * NB;
-    static_assert(N * 4 * LS <= NB * S1 * 256, "layer 1 fits its region");
-    static_assert(N * N <= NB * SH * 256, "a hidden layer fits its region");
-    static_assert(3 * N <= NB * 64, "output layer fits its region");
 };
 
 // Neuron on row `row` of an output block; the map is its own inverse.
 __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row >> 2); }
-
-__device__ __forceinline__ unsigned pack_f16(float a, float b)
-{
-    return __builtin_bit_cast(unsigned, f16x2{(_Float16)a, (_Float16)b});
-}
-
-
-// The fp16 parts of w: (w_h, w_l).
-__device__ __forceinline__ void split_weight(float w, float &h, float &l)
-{
-    const _Float16 wh = (_Float16)w;
-    h = (float)wh;
-    l = (float)(_Float16)(w - h);
-}
 
 // K entries of a layer's input: the lane group's values v_q, q < Q, times the
 // power of two sc, as the B operand of ksteps(Q) matrix steps (slot pairs as
@@ -119,36 +102,116 @@ __device__ __forceinline__ void build_b(const float (&v)[Q], float sc, u32x4 (&b
         b[s] = u32x4{reg[4 * s], reg[4 * s + 1], reg[4 * s + 2], reg[4 * s + 3]};
 }
 
-// Register w of K step s of lane (g, i) of output block ob in the A layout:
-// the packed fp16 weights that match build_b's slots.  `raw` is the layer's
-// [out][in] matrix, Q the values per lane group (input neuron or level of
-// value q: 4q + g).
-template <int Q>
-__device__ __forceinline__ unsigned a_entry(const float *raw, int fin, int fout, int ob, int s, int lane, int w,
-                                            float wsc)
+// Position (u32 index) of slot p of output neuron `out` in lane group g in a
+// layer's A layout of S K steps: block out / 16, step p / 4, lane
+// 16 g + (the row that holds out), word p % 4.
+template <int S>
+__device__ __forceinline__ int a_word(int out, int g, int p)
 {
-    // Branch-free, so that the reads of all entries a thread forms can be in
-    // flight together: an entry that holds no weight reads raw[0] and
-    // discards it.
-    constexpr int T = (Q + 1) / 2;
-    const int g = lane >> 4, out = 16 * ob + row_neuron(lane & 15);
-    const int p = 4 * s + w;
-    const bool pair = p >= Q;   // slots Q .. Q+T-1 hold the low parts of two inputs
-    const int t = p - Q;
-    const int in0 = pair ? 4 * (2 * t) + g : 4 * p + g;
-    const int in1 = 4 * (2 * t + 1) + g;
-    const bool live = out < fout && p < Q + T;
-    const bool ok0 = live && in0 < fin;
-    const bool ok1 = live && pair && 2 * t + 1 < Q && in1 < fin;
-    const float x0 = raw[ok0 ? out * fin + in0 : 0] * wsc;
-    const float x1 = raw[ok1 ? out * fin + in1 : 0] * wsc;
-    float hi0, lo0, hi1, lo1;
-    split_weight(x0, hi0, lo0);
-    split_weight(x1, hi1, lo1);
-    const float h0 = ok0 ? (pair ? lo0 : hi0) : 0.0f;
-    const float h1 = pair ? (ok1 ? lo1 : 0.0f) : h0;
-    return pack_f16(h0, h1);
+    return (((out >> 4) * S + (p >> 2)) * 64 + 16 * g + row_neuron(out & 15)) * 4 + (p & 3);
 }
+
+// A layer's weights in the A layout (slot pairs as in the header), formed a
+// work item at a time: item (out, g, t) takes inputs 4 (2t) + g and
+// 4 (2t + 1) + g of neuron `out` (zero past the layer's shape), scaled by
+// the power of two wsc and split into fp16 parts once each, and gives three
+// words: (w_h, w_h) of the first input for slot 2t, of the second for slot
+// 2t + 1 (when 2t + 1 < Q), and the pair of their w_l for slot Q + t.  The
+// slots from Q + T on are zero, so each word of the layout is written by
+// exactly one item or by the zero fill.
+//
+// Three steps, so that nothing waits for a load before every load is out:
+// load (the caller's [out][in] matrix straight from global memory, an input
+// outside the shape reading entry 0, which is a weight of the same layer and
+// so leaves the layer's maximum unchanged), max_abs, then split (once the
+// layer's scale is known; the outside inputs become zero) and store.
+template <int Q, int NB>
+struct AItems {
+    static constexpr int S = ksteps(Q);
+    static constexpr int T = (Q + 1) / 2;
+    static constexpr int ITEMS = 16 * NB * 4 * T;
+    static constexpr int PER = (ITEMS + kThreads - 1) / kThreads;
+    static constexpr int ZSLOTS = 4 * S - Q - T;   // zero slots per block and lane
+    static constexpr int ZWORDS = NB * 64 * ZSLOTS;
+    float x0[PER], x1[PER];                        // the two weights of each item, as loaded
+    unsigned hh0[PER], hh1[PER], ll[PER];          // its three words
+
+    // (out, g, t) of item it, and whether its two inputs lie in the shape
+    __device__ static void decode(int it, int fin, int fout, int &out, int &g, int &t, bool &ok0, bool &ok1)
+    {
+        g = it & 3;
+        t = (it >> 2) % T;
+        out = (it >> 2) / T;
+        ok0 = out < fout && 8 * t + g < fin;
+        ok1 = out < fout && 2 * t + 1 < Q && 8 * t + 4 + g < fin;
+    }
+
+    // (a thread past the last item repeats it: its values count once more
+    // in the maximum and are not stored)
+    __device__ void load(const float *w, int fin, int fout)
+    {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int it0 = (int)threadIdx.x + k * kThreads;
+            int out, g, t;
+            bool ok0, ok1;
+            decode(it0 < ITEMS ? it0 : ITEMS - 1, fin, fout, out, g, t, ok0, ok1);
+            x0[k] = w[ok0 ? out * fin + 8 * t + g : 0];
+            x1[k] = w[ok1 ? out * fin + 8 * t + 4 + g : 0];
+        }
+    }
+
+    __device__ float max_abs() const
+    {
+        float m = 0.0f;
+#pragma unroll
+        for (int k = 0; k < PER; ++k)
+            m = fmaxf(m, fmaxf(fabsf(x0[k]), fabsf(x1[k])));
+        return m;
+    }
+
+    __device__ void split(int fin, int fout, float wsc)
+    {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int it0 = (int)threadIdx.x + k * kThreads;
+            int out, g, t;
+            bool ok0, ok1;
+            decode(it0 < ITEMS ? it0 : ITEMS - 1, fin, fout, out, g, t, ok0, ok1);
+            const float a = ok0 ? x0[k] * wsc : 0.0f, c = ok1 ? x1[k] * wsc : 0.0f;
+            const _Float16 h0 = (_Float16)a, h1 = (_Float16)c;
+            const _Float16 l0 = (_Float16)(a - (float)h0), l1 = (_Float16)(c - (float)h1);
+            hh0[k] = __builtin_bit_cast(unsigned, f16x2{h0, h0});
+            hh1[k] = __builtin_bit_cast(unsigned, f16x2{h1, h1});
+            ll[k] = __builtin_bit_cast(unsigned, f16x2{l0, l1});
+        }
+    }
+
+    __device__ void store(unsigned *dst) const
+    {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int it = (int)threadIdx.x + k * kThreads;
+            if (it < ITEMS) {
+                const int g = it & 3, t = (it >> 2) % T, out = (it >> 2) / T;
+                dst[a_word<S>(out, g, 2 * t)] = hh0[k];
+                if (2 * t + 1 < Q)
+                    dst[a_word<S>(out, g, 2 * t + 1)] = hh1[k];
+                dst[a_word<S>(out, g, Q + t)] = ll[k];
+            }
+        }
+        if constexpr (ZSLOTS > 0) {
+#pragma unroll
+            for (int z0 = 0; z0 < ZWORDS; z0 += kThreads) {
+                const int z = z0 + (int)threadIdx.x;
+                if (z < ZWORDS) {
+                    const int bl = z / ZSLOTS, p = Q + T + z % ZSLOTS;   // bl: block * 64 + lane
+                    dst[(((bl >> 6) * S + (p >> 2)) * 64 + (bl & 63)) * 4 + (p & 3)] = 0u;
+                }
+            }
+        }
+    }
+};
 
 __device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
@@ -185,24 +248,23 @@ __device__ __forceinline__ float input_scale(const float (&v)[Q], float &inv)
     return scale_for(column_max(m), inv);
 }
 
-// Largest magnitude in a part (this thread's entries).
-template <int COUNT>
-__device__ __forceinline__ float part_max(const Part<COUNT, float> &r)
-{
-    float m = 0.0f;
-#pragma unroll
-    for (int i = 0; i < Part<COUNT, float>::kPer; ++i)
-        m = fmaxf(m, fabsf(r.v[i]));
-    return m;
-}
-
-// Largest of x over the wavefront.
+// Largest of x (>= 0, not NaN: such floats order like their bit patterns)
+// over the wavefront, by data-parallel moves within the vector unit instead
+// of exchanges through LDS: the maximum of each quad (two quad
+// permutations), of each row of 16 (row shifts by 4 and 8 leave it in lane
+// 15), then of rows 0-1 and 2-3 (lane 15 of the row before broadcast into
+// rows 1 and 3) and of the wavefront (lane 31 broadcast into rows 2 and 3),
+// read from lane 63.  Lanes a move does not write keep their own value.
 __device__ __forceinline__ float wave_max(float x)
 {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1)
-        x = fmaxf(x, __shfl_xor(x, d, 64));
-    return x;
+    int v = __float_as_int(x);
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));    // quad_perm [1, 0, 3, 2]
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));    // quad_perm [2, 3, 0, 1]
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x114, 0xF, 0xF, false));   // row_shr:4
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x118, 0xF, 0xF, false));   // row_shr:8
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x142, 0xA, 0xF, false));   // row_bcast:15, rows 1 and 3
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x143, 0xC, 0xF, false));   // row_bcast:31, rows 2 and 3
+    return __int_as_float(__builtin_amdgcn_readlane(v, 63));
 }
 
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: levels per
@@ -241,15 +303,12 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     if (blk < tiles)
         load_boxes<4 * LS, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
 
-    // ---- this image's parameters: contiguous loads (all in flight at once)
-    // into LDS as the caller lays them out, then scaled, split into fp16
-    // parts and permuted into the operand layouts through registers
+    // ---- this image's parameters, loaded straight into their operand
+    // layouts' order (all loads in flight at once); each layer's largest
+    // weight magnitude gives its scale, after one barrier the weights are
+    // split into fp16 parts and stored
     float wsc[NH + 1], winv[NH + 1];
     {
-        // every layer's pointers and widths first (one batch of scalar
-        // loads), then the raw copies, branch-free (entries past a layer's
-        // size repeat its last entry: the maxima are unchanged and the
-        // permutation reads only valid ones)
         LayerParams lp[NH + 2];
         int wd[NH + 3];
 #pragma unroll
@@ -259,26 +318,38 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
         for (int l = 0; l < NH + 3; ++l)
             wd[l] = p.widths[l];
         const int N1 = wd[1], NL = wd[NH + 1];
-        const auto r1 = load_part<LY::N * 4 * LS, float>([&](int s) { return lp[0].template weight_clamped<false>(s, N1 * L); });
-        Part<LY::N * LY::N, float> rh[NH > 0 ? NH : 1];
+        AItems<LS, NB> w1a;                                                    // layer 1
+        w1a.load(static_cast<const float *>(lp[0].w), L, N1);
+        AItems<KSH, NB> wha[NH > 0 ? NH : 1];
 #pragma unroll
-        for (int h = 0; h < NH; ++h) {
-            const int n = wd[1 + h] * wd[2 + h];
-            rh[h] = load_part<LY::N * LY::N, float>([&](int s) { return lp[1 + h].template weight_clamped<false>(s, n); });
-        }
-        const auto r3 = load_part<3 * LY::N, float>([&](int s) { return lp[NH + 1].template weight_clamped<false>(s, 3 * NL); });
-        Part<LY::N, float> rb[NH + 1];
+        for (int h = 0; h < NH; ++h)                                            // hidden layers
+            wha[h].load(static_cast<const float *>(lp[1 + h].w), wd[1 + h], wd[2 + h]);
+        // biases in swz order (position s holds neuron swz(s)), the output
+        // layer as [ob][r][g][c] (neuron 16 ob + 4 r + g, channel c): raw
+        // loads (an entry outside the shape reads entry 0), zeroed when stored
+        constexpr int BPER = (LY::N + kThreads - 1) / kThreads, WPER = (NB * 64 + kThreads - 1) / kThreads;
+        float braw[NH + 1][BPER], w3raw[WPER];
 #pragma unroll
-        for (int h = 0; h <= NH; ++h) {
-            const int fout = wd[1 + h];
-            rb[h] = load_part<LY::N, float>([&](int s) { return lp[h].bias_clamped(s, fout); });
+        for (int h = 0; h <= NH; ++h)
+#pragma unroll
+            for (int k = 0; k < BPER; ++k) {
+                const int s = min((int)threadIdx.x + k * kThreads, LY::N - 1);
+                const int n = (s & ~15) | ((s & 3) << 2) | ((s >> 2) & 3);
+                braw[h][k] = lp[h].b[n < wd[1 + h] ? n : 0];
+            }
+        const float *w3p = static_cast<const float *>(lp[NH + 1].w);
+#pragma unroll
+        for (int k = 0; k < WPER; ++k) {
+            const int s = min((int)threadIdx.x + k * kThreads, NB * 64 - 1);
+            const int c = s & 3, n = 16 * (s >> 6) + 4 * ((s >> 4) & 3) + ((s >> 2) & 3);
+            w3raw[k] = w3p[c < 3 && n < NL ? c * NL + n : 0];
         }
         {
-            const float m1 = wave_max(part_max(r1));
+            const float m1 = wave_max(w1a.max_abs());
             float mh[NH > 0 ? NH : 1];
 #pragma unroll
             for (int h = 0; h < NH; ++h)
-                mh[h] = wave_max(part_max(rh[h]));
+                mh[h] = wave_max(wha[h].max_abs());
             if (lane == 0) {
                 lds[LY::WSC + wave] = m1;
 #pragma unroll
@@ -286,14 +357,24 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                     lds[LY::WSC + (1 + h) * kWaves + wave] = mh[h];
             }
         }
-        store_part(lds + LY::W1A, r1);
-#pragma unroll
-        for (int h = 0; h < NH; ++h)
-            store_part(lds + LY::WHA + h * NB * SH * 256, rh[h]);
-        store_part(lds + LY::W3, r3);
 #pragma unroll
         for (int h = 0; h <= NH; ++h)
-            store_part(lds + LY::B1 + h * NB * 256, rb[h]);
+#pragma unroll
+            for (int k = 0; k < BPER; ++k) {
+                const int s = (int)threadIdx.x + k * kThreads;
+                const int n = (s & ~15) | ((s & 3) << 2) | ((s >> 2) & 3);
+                if (s < LY::N)
+                    lds[LY::B1 + h * LY::N + s] = n < wd[1 + h] ? braw[h][k] : 0.0f;
+            }
+#pragma unroll
+        for (int k = 0; k < WPER; ++k) {
+            const int s = (int)threadIdx.x + k * kThreads;
+            const int c = s & 3, n = 16 * (s >> 6) + 4 * ((s >> 4) & 3) + ((s >> 2) & 3);
+            if (s < NB * 64)
+                lds[LY::W3 + s] = c < 3 && n < NL ? w3raw[k] : 0.0f;
+        }
+        if (blk < tiles)
+            store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
         __syncthreads();
         // each layer's weight scale and its inverse (wave-uniform)
 #pragma unroll
@@ -301,47 +382,14 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
             const float *m = lds + LY::WSC + h * kWaves;
             wsc[h] = scale_for(fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3])), winv[h]);
         }
-
-        const auto w1a = load_part<NB * S1 * 256, unsigned>([&](int s) {      // layer 1, A layout
-            const int w = s & 3, ln = (s >> 2) & 63, st = (s >> 8) % S1, ob = (s >> 8) / S1;
-            return a_entry<LS>(lds + LY::W1A, L, N1, ob, st, ln, w, wsc[0]);
-        });
-        Part<NB * SH * 256, unsigned> wha[NH > 0 ? NH : 1];
+        w1a.split(L, N1, wsc[0]);
+        w1a.store(ldsu + LY::W1A);
 #pragma unroll
-        for (int h = 0; h < NH; ++h) {                                         // hidden layers, A layout
-            const int fin = p.widths[1 + h], fout = p.widths[2 + h];
-            wha[h] = load_part<NB * SH * 256, unsigned>([&](int s) {
-                const int w = s & 3, ln = (s >> 2) & 63, st = (s >> 8) % SH, ob = (s >> 8) / SH;
-                return a_entry<KSH>(lds + LY::WHA + h * NB * SH * 256, fin, fout, ob, st, ln, w, wsc[1 + h]);
-            });
+        for (int h = 0; h < NH; ++h) {
+            wha[h].split(wd[1 + h], wd[2 + h], wsc[1 + h]);
+            wha[h].store(ldsu + LY::WHA + h * NB * SH * 256);
         }
-        Part<NB * 256, float> bias[NH + 1];
-#pragma unroll
-        for (int h = 0; h <= NH; ++h) {                                        // biases, accumulator layout
-            const int fout = p.widths[1 + h];
-            bias[h] = load_part<NB * 256, float>([&](int s) {
-                const int r = s & 3, ln = (s >> 2) & 63, ob = s >> 8;
-                const int n = 16 * ob + 4 * r + (ln >> 4);
-                return lds_or_zero(lds + LY::B1 + h * NB * 256, n < fout, n);
-            });
-        }
-        const auto w3 = load_part<NB * 64, float>([&](int s) {                // output layer [ob][r][g][c]
-            const int c = s & 3, gg = (s >> 2) & 3, r = (s >> 4) & 3, ob = s >> 6;
-            const int n = 16 * ob + 4 * r + gg;
-            return lds_or_zero(lds + LY::W3, c < 3 && n < NL, c * NL + n);
-        });
-        __syncthreads();                   // every raw value is read
-        store_part(ldsu + LY::W1A, w1a);
-#pragma unroll
-        for (int h = 0; h < NH; ++h)
-            store_part(ldsu + LY::WHA + h * NB * SH * 256, wha[h]);
-#pragma unroll
-        for (int h = 0; h <= NH; ++h)
-            store_part(lds + LY::B1 + h * NB * 256, bias[h]);
-        store_part(lds + LY::W3, w3);
     }
-    if (blk < tiles)
-        store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
     __syncthreads();
 
     // ---- the level each lane samples as its value q of the first layer:
@@ -426,12 +474,17 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                         const u32x4 a = *reinterpret_cast<const u32x4 *>(&ldsu[LY::W1A + ((ob * S1 + s) * 64 + lane) * 4]);
                         d[ob] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_f16x8(a), as_f16x8(b1[s]), d[ob], 0, 0, 0);
                     }
-                // unscale, add the bias, ReLU
+                // unscale, add the bias, ReLU (the biases of a block's four
+                // registers: one 16-byte read, the same for the lane group)
                 float v[KSH];
 #pragma unroll
-                for (int q = 0; q < KSH; ++q)
-                    v[q] = relu(__builtin_fmaf(d[q >> 2][q & 3], un1,
-                                               lds[LY::B1 + ((q >> 2) * 64 + lane) * 4 + (q & 3)]));
+                for (int ob = 0; ob < (KSH + 3) / 4; ++ob) {
+                    const f32x4 bb = *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + 16 * ob + 4 * g]);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (4 * ob + r < KSH)
+                            v[4 * ob + r] = relu(__builtin_fmaf(d[ob][r], un1, bb[r]));
+                }
 
                 // hidden layers
 #pragma unroll
@@ -455,9 +508,14 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                                                                           0);
                         }
 #pragma unroll
-                    for (int q = 0; q < KSH; ++q)
-                        v[q] = relu(__builtin_fmaf(e[q >> 2][q & 3], unh,
-                                                   lds[LY::BH + ((h * NB + (q >> 2)) * 64 + lane) * 4 + (q & 3)]));
+                    for (int ob = 0; ob < (KSH + 3) / 4; ++ob) {
+                        const f32x4 bb =
+                            *reinterpret_cast<const f32x4 *>(&lds[LY::B1 + (1 + h) * LY::N + 16 * ob + 4 * g]);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (4 * ob + r < KSH)
+                                v[4 * ob + r] = relu(__builtin_fmaf(e[ob][r], unh, bb[r]));
+                    }
                 }
 
                 // output layer on the vector ALU: partial sums over this lane's
