@@ -70,7 +70,9 @@ typedef enum pic_dtype {
 } pic_dtype;
 
 /* Kernel family.  AUTO picks MFMA_F32 for fp32 weights and MFMA_BF16 for
- * bf16 weights where that family covers the shape, VALU otherwise.  VALU is
+ * bf16 weights where that family covers the shape, VALU otherwise, and VALU
+ * also for fp32 nets whose hidden layers are all at most 8 wide (the matrix
+ * family would pad them to 16-neuron blocks).  VALU is
  * the reference family: plain binary32 arithmetic in a
  * fixed order (bias first, then one fused multiply-add per input in
  * increasing index), so its results are reproducible bit for bit. */

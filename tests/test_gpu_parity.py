@@ -408,6 +408,25 @@ def test_bf16_family_u8_band():
     assert diff.max() <= 2
 
 
+# ------------------------------------------------- AUTO on narrow fp32 nets
+
+@pytest.mark.parametrize("widths,want", [
+    ((8, 8, 8, 8, 3), "valu"), ((4, 8, 3), "valu"), ((7, 5, 8, 3), "valu"),
+    ((8, 9, 3), "mfma_f32"), ((8, 8, 16, 3), "mfma_f32"), ((8, 16, 16, 16, 3), "mfma_f32")])
+def test_auto_family_for_narrow_nets(widths, want):
+    """AUTO runs fp32 nets whose hidden layers are all at most 8 wide on the
+    vector family (the matrix family pads them to 16-neuron blocks), wider
+    ones on the fp32 matrix family; the result matches the oracle either
+    way (200x300, ragged against the tiles)."""
+    inp = synth.make_inputs(200, 300, widths[0], widths, batch=2, seed=31, latent_scale=1.5, bias="normal")
+    got, info = gpu_decode(inp, clamp=False)
+    assert info["variant"] == want
+    ref = oracle.decode_inputs(inp, out="raw")
+    err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
+    print(f"PARITY auto {widths} -> {want}: max err {err:.3e}", flush=True)
+    assert err <= TOL
+
+
 # ------------------------------------------ per-layer parameters, App. A fusion
 
 def test_run_layers_shared_and_per_image():
