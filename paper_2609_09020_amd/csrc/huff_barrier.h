@@ -3,14 +3,17 @@
 // to arrive runs a serial step (the repair of subsequences a workgroup could
 // not settle) and then releases the others, which wait for it a bounded time.
 //
-// State: one 64-bit word, generation << 32 | arrivals, zero when the handle
-// is created.  A workgroup arrives with one atomic add, which also returns
-// the generation it arrived in.  The last arrival (arrivals == n - 1) owns
-// the serial step; when done it stores (generation + 1) << 32: the count is
-// back at zero for the next launch, and the waiters, spinning on the
-// generation, go on.  Nothing is cleared between launches (a replayed launch
-// finds the word as the previous one left it), and a waiter that gives up
-// leaves the word consistent: the last arrival still resets it.
+// State: one 64-bit word, generation << 32 | flagged << 16 | arrivals, zero
+// when the handle is created.  A workgroup arrives with one atomic add, which
+// also returns the generation it arrived in; a workgroup that has something
+// for the serial step adds one to `flagged` in the same add.  The last
+// arrival (arrivals == n - 1) owns the serial step and learns from the value
+// it read whether any workgroup flagged one; when done it stores
+// (generation + 1) << 32: count and flags are back at zero for the next
+// launch, and the waiters, spinning on the generation, go on.  Nothing is
+// cleared between launches (a replayed launch finds the word as the previous
+// one left it), and a waiter that gives up leaves the word consistent: the
+// last arrival still resets it.  At most 65535 workgroups arrive.
 //
 // The last arrival can only come once every workgroup has started: a waiter
 // that holds a CU while others of the launch wait for one could wait for
@@ -49,17 +52,20 @@ namespace huff_barrier {
 struct Arrival {
     uint32_t generation;   // the generation the caller arrived in
     bool last;             // the caller arrived last: it owns the serial step
+    bool flagged;          // (last only) some workgroup, the caller included, flagged
 };
 
 // Arrive; one call per workgroup and launch.  `n` is the number of
-// workgroups of the launch (>= 1).
+// workgroups of the launch (1 .. 65535); `flag`: the caller has something
+// for the serial step.
 template <class Ops>
-PIC_HD inline Arrival arrive(uint64_t *word, uint32_t n)
+PIC_HD inline Arrival arrive(uint64_t *word, uint32_t n, bool flag)
 {
-    const uint64_t old = Ops::fetch_add(word, 1u);
+    const uint64_t old = Ops::fetch_add(word, flag ? 0x10001u : 1u);
     Arrival a;
     a.generation = (uint32_t)(old >> 32);
-    a.last = (uint32_t)old == n - 1u;
+    a.last = (old & 0xffffu) == n - 1u;
+    a.flagged = flag || ((old >> 16) & 0xffffu) != 0;
     return a;
 }
 

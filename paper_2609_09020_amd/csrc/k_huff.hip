@@ -444,9 +444,12 @@ __device__ __forceinline__ int32_t block_sum_incl(int32_t v, int32_t *s_wsum, in
 
 // The parse of a workgroup's subsequences, the in-step check and repair, and
 // its records.  All threads; the tables and the staged words are ready in LDS.
+// The workgroup's summary word (what the repair step has to look at: 0 when
+// nothing) also goes to *s_summary, visible to the workgroup after its next
+// barrier.
 __device__ __forceinline__ void parse_phase(const HuffParams &p, const SharedTables &s_tab,
                                             const uint32_t *s_words, int32_t *s_end, int32_t *s_moved,
-                                            int32_t *s_wsum, int blk)
+                                            int32_t *s_wsum, int blk, int32_t *s_summary)
 {
     const int l = threadIdx.x;
     const int32_t t0 = blk * kHuffOwn;           // first owned subsequence
@@ -527,8 +530,11 @@ __device__ __forceinline__ void parse_phase(const HuffParams &p, const SharedTab
         p.blk[blk] = total;
     // bit 0: the next workgroup took this one's last nominal crossing point,
     // and it moved; bit 1: a subsequence here was left to the fix kernel
-    if (l == kHuffThreads - 1)
-        p.bnd[blk] = (live && end != nominal_end ? 1 : 0) | (any_bad ? 2 : 0);
+    if (l == kHuffThreads - 1) {
+        const int32_t summary = (live && end != nominal_end ? 1 : 0) | (any_bad ? 2 : 0);
+        p.bnd[blk] = summary;
+        *s_summary = summary;
+    }
 }
 
 __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
@@ -556,7 +562,8 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_parse(HuffParams p)
     build_lut(s_tab);
     store_words(s_words, sw);
     __syncthreads();
-    parse_phase(p, s_tab, s_words, s_end, s_moved, s_wsum, (int)blockIdx.x);
+    __shared__ int32_t s_summary;
+    parse_phase(p, s_tab, s_words, s_end, s_moved, s_wsum, (int)blockIdx.x, &s_summary);
 }
 
 // Walk subsequence u again from the true crossing point of its predecessor
@@ -896,7 +903,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
         int32_t vals[kWriteLds];
     } s_u;
     __shared__ int32_t s_wsum[kWaves];
-    __shared__ int32_t s_last, s_ok;
+    __shared__ int32_t s_last, s_ok, s_flagged, s_summary;
     __shared__ uint32_t s_gen;
     const int l = threadIdx.x;
     const int blk = (int)blockIdx.x;
@@ -915,7 +922,7 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
         build_lut(s_tab);
         store_words(s_words, sw);
         __syncthreads();
-        parse_phase(p, s_tab, s_words, s_u.parse.end, s_u.parse.moved, s_wsum, blk);
+        parse_phase(p, s_tab, s_words, s_u.parse.end, s_u.parse.moved, s_wsum, blk, &s_summary);
     }
     // hand-off: every workgroup arrives, also with an invalid table, so that
     // the word's count comes back to zero.  Each wavefront waits for its
@@ -927,25 +934,36 @@ __global__ __launch_bounds__(kHuffThreads) void k_huff_one(HuffParams p)
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (l == 0) {
-        const huff_barrier::Arrival a = huff_barrier::arrive<huff_barrier::DeviceOps>(p.sync, (uint32_t)p.nblk);
+        // flagged: this workgroup left something to the repair step (with an
+        // invalid table nothing was parsed and there is nothing to repair)
+        const huff_barrier::Arrival a =
+            huff_barrier::arrive<huff_barrier::DeviceOps>(p.sync, (uint32_t)p.nblk, valid && s_summary != 0);
         s_last = a.last;
+        s_flagged = a.flagged;
         s_gen = a.generation;
     }
     __syncthreads();
     huff_barrier::Arrival a;
     a.generation = s_gen;
     a.last = s_last != 0;
+    a.flagged = s_flagged != 0;
     if (a.last) {                          // uniform
-        // one invalidate per workgroup: its wavefronts share one CU
-        if (l < 64)
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        __syncthreads();
-        fix_phase(p, s_tab, valid, s_u.list, s_wsum);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (l < 64)
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        __syncthreads();
+        // The repair step only when a workgroup flagged it (a moved crossing
+        // point or a subsequence it could not settle); otherwise the last
+        // arrival reads and writes nothing the others need, so it releases
+        // at once, without the fences.
+        if (a.flagged) {                   // uniform
+            // one invalidate per workgroup: its wavefronts share one CU
+            if (l < 64)
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            __syncthreads();
+            fix_phase(p, s_tab, valid, s_u.list, s_wsum);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            if (l < 64)
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __syncthreads();
+        }
         if (l == 0)
             huff_barrier::release<huff_barrier::DeviceOps>(p.sync, a);
     } else {

@@ -45,22 +45,26 @@ struct HostOps {
 // largest poll count of a waiter.
 struct Outcome {
     int released = 0, gave_up = 0, saw_payload = 0, lasts = 0;
+    bool last_flagged = false;
     unsigned long long max_polls = 0;
 };
 
+// flags: bit i set when workgroup i (< 64) flags something for the serial step
 static Outcome launch(uint64_t *word, int n, uint32_t spin_limit, int delay_ms, bool no_release,
-                      int *payload, int value)
+                      int *payload, int value, uint64_t flags = 0)
 {
     Outcome o;
     std::atomic<int> released{0}, gave_up{0}, saw{0}, lasts{0};
+    std::atomic<bool> last_flagged{false};
     std::atomic<unsigned long long> maxp{0};
     std::vector<std::thread> ts;
     for (int i = 0; i < n; ++i)
-        ts.emplace_back([&] {
+        ts.emplace_back([&, i] {
             polls = 0;
-            const hb::Arrival a = hb::arrive<HostOps>(word, (uint32_t)n);
+            const hb::Arrival a = hb::arrive<HostOps>(word, (uint32_t)n, i < 64 && ((flags >> i) & 1u));
             if (a.last) {
                 ++lasts;
+                last_flagged = a.flagged;
                 if (delay_ms)
                     std::this_thread::sleep_for(std::chrono::milliseconds(delay_ms));
                 __atomic_store_n(payload, value, __ATOMIC_SEQ_CST);
@@ -85,6 +89,7 @@ static Outcome launch(uint64_t *word, int n, uint32_t spin_limit, int delay_ms, 
     o.gave_up = gave_up;
     o.saw_payload = saw;
     o.lasts = lasts;
+    o.last_flagged = last_flagged;
     o.max_polls = maxp;
     return o;
 }
@@ -135,7 +140,24 @@ int main()
         CHECK(o.max_polls == lim, "polls %llu", o.max_polls);
         std::printf("bound: 7 waiters gave up after %llu polls each (limit %u)\n", o.max_polls, lim);
     }
-    // 5. leaving: every workgroup once, some with error bits; exactly one
+    // 5. flags: the last arrival learns whether any workgroup (itself
+    //    included, whichever arrives last) flagged the serial step, and the
+    //    release clears the flags with the count
+    {
+        uint64_t fword = 0, gen = 0;   // (the bound above left its word unreleased on purpose)
+        const uint64_t patterns[] = {0ull, 1ull, 1ull << 63, 0x5555555555555555ull, ~0ull, 1ull << 17};
+        for (int g = 0; g < 120; ++g) {
+            const int n = 1 + g % 64;
+            const uint64_t f = patterns[g % 6] & (n == 64 ? ~0ull : ((1ull << n) - 1));
+            const Outcome o = launch(&fword, n, 1u << 30, 0, false, &payload, 300 + g, f);
+            CHECK(o.lasts == 1 && o.released == n - 1, "flag launch %d", g);
+            CHECK(o.last_flagged == (f != 0), "launch %d: flagged %d, want %d", g, (int)o.last_flagged, (int)(f != 0));
+            ++gen;
+            CHECK(fword == gen << 32, "launch %d: word %llx", g, (unsigned long long)fword);
+        }
+        std::printf("flags: 120 launches of 1..64 workgroups, the last arrival saw every flag, word reset\n");
+    }
+    // 6. leaving: every workgroup once, some with error bits; exactly one
     //    last, which gets every bit, and the word is zero again; repeated
     {
         uint64_t leave_word = 0;
