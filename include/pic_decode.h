@@ -140,7 +140,9 @@ typedef struct pic_decode_info {
  * dtypes, flags out of range); PIC_E_UNSUPPORTED for a valid combination no
  * kernel implements (e.g. MFMA_BF16 with fp32 weights); PIC_E_NODEVICE when no
  * gfx950 device is current; PIC_E_NOMEM when the handle cannot be allocated;
- * PIC_E_HIP when its device memory cannot (allocated and cleared here, once).
+ * PIC_E_HIP when its device memory cannot (allocated and cleared here, once;
+ * the clear runs on a private stream and waits for itself alone, not for work
+ * queued on other streams).
  * Defines: Sec. 3.1 (pyramid and upsample), Sec. 4.1 / App. A (MLP).
  */
 PIC_API pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out);

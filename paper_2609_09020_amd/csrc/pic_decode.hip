@@ -185,8 +185,7 @@ pic_status pic_decode_create(const pic_decode_desc *desc, pic_decoder **out)
     init_handle(d, desc, variant, dev, num_cus);
     const size_t ctr_bytes = sizeof(int32_t) * 2 * (size_t)pic::tile_counters(desc->max_batch);
     void *mem = nullptr;
-    if (hipMalloc(&mem, ctr_bytes) != hipSuccess || hipMemset(mem, 0, ctr_bytes) != hipSuccess ||
-        hipDeviceSynchronize() != hipSuccess) {
+    if (hipMalloc(&mem, ctr_bytes) != hipSuccess || pic::zero_device_memory(mem, ctr_bytes) != hipSuccess) {
         (void)hipGetLastError();
         if (mem)
             (void)hipFree(mem);

@@ -87,8 +87,7 @@ pic_status pic_huff_create(const pic_huff_desc *d, pic_huff **out)
     h->d_scratch = static_cast<char *>(mem);
     // the one-launch path's hand-off word starts at zero; each launch leaves
     // it ready for the next
-    if (hipMemset(h->d_scratch + h->o_sync, 0, 2 * sizeof(uint64_t)) != hipSuccess ||
-        hipDeviceSynchronize() != hipSuccess) {
+    if (pic::zero_device_memory(h->d_scratch + h->o_sync, 2 * sizeof(uint64_t)) != hipSuccess) {
         (void)hipGetLastError();
         (void)hipFree(mem);
         delete h;

@@ -28,6 +28,22 @@ __device__ __forceinline__ void warm_kernel_args()
                  "s"(v[8]), "s"(v[9]), "s"(v[10]), "s"(v[11]));
 }
 
+// Zero `bytes` of device memory and wait for that alone: on a private
+// non-blocking stream (default priority), so that work already queued on the
+// caller's streams is not waited for.  For handle set-up, never inside a
+// captured stream.
+inline hipError_t zero_device_memory(void *mem, size_t bytes)
+{
+    hipStream_t s = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    if (e != hipSuccess)
+        return e;
+    e = hipMemsetAsync(mem, 0, bytes, s);
+    const hipError_t w = hipStreamSynchronize(s);
+    const hipError_t d = hipStreamDestroy(s);
+    return e != hipSuccess ? e : (w != hipSuccess ? w : d);
+}
+
 // Tile counters a decode handle keeps per run: one per image, and at least
 // one per XCD (a one-image grid schedules each XCD's tiles separately).
 constexpr int kXcds = 8;

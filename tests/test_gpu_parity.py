@@ -353,6 +353,33 @@ def test_runs_on_caller_stream():
     assert np.array_equal(got, ref)
 
 
+def test_create_does_not_wait_for_other_streams():
+    """Creating a decode or an entropy-decoding handle clears its device
+    memory on a private stream and waits for that alone: about 50 ms of
+    decodes queued on another stream are still running when both creates
+    return (an event recorded after them has not completed)."""
+    from paper_2609_09020_amd import Decoder, HuffDecoder
+    inp = synth.workload_inputs(synth.WORKLOADS["uhd4k"])
+    lat, w, b = _to_dev(inp)
+    dec = Decoder(inp.height, inp.width, inp.widths, max_batch=1, variant="mfma_f32")
+    out = dec.alloc_out(1, "cuda")
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    done = torch.cuda.Event()
+    with torch.cuda.stream(s):
+        for _ in range(80):                  # 0.6 ms each
+            dec.run(lat, w, b, out=out, stream=s.cuda_stream)
+        done.record(s)
+    d2 = Decoder(512, 768, (7, 40, 40, 3), max_batch=4)
+    h2 = HuffDecoder(1 << 20)
+    pending = not done.query()
+    torch.cuda.synchronize()
+    d2.close()
+    h2.close()
+    dec.close()
+    assert pending, "a handle's creation waited for work queued on another stream"
+
+
 def test_run_rejects_bad_arguments_before_launch():
     from paper_2609_09020_amd import decoder as D
     inp = synth.make_inputs(8, 8, 2, (2, 4, 3), batch=2, seed=0)
