@@ -170,23 +170,24 @@ __device__ void build_lut(SharedTables &s)
 {
     constexpr int kPer = kLut / kHuffThreads;
     uint32_t lim[kHuffLutBits + 1];
-    int32_t fc[kHuffLutBits + 1], fi[kHuffLutBits + 1];
 #pragma unroll
-    for (int l = 1; l <= kHuffLutBits; ++l) {
+    for (int l = 1; l <= kHuffLutBits; ++l)
         lim[l] = s.lim[l];
-        fc[l] = s.fc[l];
-        fi[l] = s.fi[l];
-    }
     uint32_t ent[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
         const int k = threadIdx.x + j * kHuffThreads;
         const uint32_t v = (uint32_t)k << (kHuffMaxLen - kHuffLutBits);
-        uint32_t e = 0;
+        // The limits grow with the length, so the first codeword's length is
+        // one more than the number of limits at or below v (12: longer than
+        // the table's bits); its index is its code plus d[length].
+        int c = 0;
 #pragma unroll
-        for (int l = kHuffLutBits; l >= 1; --l)
-            if (v < lim[l])
-                e = (uint32_t)(fi[l] + (k >> (kHuffLutBits - l)) - fc[l]) | (uint32_t)l << 16;
+        for (int l = 1; l <= kHuffLutBits; ++l)
+            c += v >= lim[l] ? 1 : 0;
+        const int len = c < kHuffLutBits ? c + 1 : kHuffLutBits;
+        const uint32_t idx = (uint32_t)(s.d[len] + (k >> (kHuffLutBits - len)));
+        const uint32_t e = c < kHuffLutBits ? idx | (uint32_t)len << 16 : 0u;
         ent[j] = e;
         s.lut[k] = e;
     }
