@@ -136,19 +136,22 @@ __device__ void build_code(const HuffParams &p, SharedTables &s, int len0)
         // themselves; clamped so the sums stay in 32 bits
         const uint32_t w = t >= 1 && t <= kHuffMaxLen
                                ? (uint32_t)min(c, (1 << t) + 1) << (kHuffMaxLen - t) : 0u;
-        int32_t fi = c;
-        uint32_t lim = w;
-#pragma unroll
-        for (int d = 1; d < 32; d <<= 1) {
-            const int32_t a = __shfl_up(fi, d, 32);
-            const uint32_t b = __shfl_up(lim, d, 32);
-            if (t >= d) {
-                fi += a;
-                lim += b;
-            }
-        }
+        // inclusive sums over lanes 0..31 by data-parallel moves: shifts by
+        // 1, 2, 4, 8 within each row of 16 lanes (a lane with no source adds
+        // 0), then row 0's total into row 1
+        auto prefix = [](uint32_t x) {
+            x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);   // row_shr:1
+            x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);   // row_shr:2
+            x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);   // row_shr:4
+            x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);   // row_shr:8
+            x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);   // row_bcast:15
+            return x;
+        };
+        int32_t fi = (int32_t)prefix((uint32_t)c);
+        const uint32_t lim = prefix(w);
         fi -= c;                           // exclusive
-        const uint32_t below = __shfl_up(lim, 1, 32);
+        // lim of the lane before (wave_shr:1; lane 0 reads 0 and is not used)
+        const uint32_t below = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lim, 0x138, 0xF, 0xF, false);
         const int32_t fc = t >= 1 ? (int32_t)(below >> (kHuffMaxLen - t)) : 0;
         if (t <= kHuffMaxLen) {
             s.fi[t] = fi;
