@@ -425,13 +425,7 @@ __device__ __forceinline__ int32_t crossing(int state, int32_t pos, int32_t n_bi
 __device__ __forceinline__ int32_t block_sum_incl(int32_t v, int32_t *s_wsum, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int32_t incl = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int32_t o = __shfl_up(incl, d, 64);
-        if (lane >= d)
-            incl += o;
-    }
+    const int32_t incl = wave_inclusive_sum(v);
     if (lane == 63)
         s_wsum[wave] = incl;
     __syncthreads();

@@ -83,13 +83,7 @@ __host__ __device__ constexpr float dct_basis(int x, int v)
 __device__ __forceinline__ int32_t block_inclusive_sum(int32_t v, int32_t *s_wsum, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int32_t incl = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int32_t o = __shfl_up(incl, d, 64);
-        if (lane >= d)
-            incl += o;
-    }
+    const int32_t incl = wave_inclusive_sum(v);
     if (lane == 63)
         s_wsum[wave] = incl;
     __syncthreads();
@@ -167,13 +161,7 @@ __global__ __launch_bounds__(kScanThreads) void k_zpr_scan(ZprParams p)
             v[j] = s_seg[t * kScanPer + j];
             sum += v[j];
         }
-        int32_t incl = sum;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int32_t o = __shfl_up(incl, d, 64);
-            if (lane >= d)
-                incl += o;
-        }
+        const int32_t incl = wave_inclusive_sum(sum);
         if (lane == 63)
             s_wsum[wave] = incl;
         __syncthreads();

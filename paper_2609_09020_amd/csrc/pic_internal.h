@@ -28,6 +28,24 @@ __device__ __forceinline__ void warm_kernel_args()
                  "s"(v[8]), "s"(v[9]), "s"(v[10]), "s"(v[11]));
 }
 
+// Inclusive sum of x over the 64 lanes of the wavefront (every lane active),
+// by data-parallel moves between lanes instead of exchanges through LDS:
+// shifts by 1, 2, 4 and 8 within each row of 16 lanes give each row's
+// running sums (a lane with no source adds 0); then lane 15 into row 1 and
+// lane 47 into row 3, and lane 31 into rows 2 and 3, carry the earlier rows'
+// totals.  Sums wrap like integer additions (packed counters stay packed
+// while no field overflows).
+__device__ __forceinline__ int32_t wave_inclusive_sum(int32_t x)
+{
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);   // row_bcast:15, rows 1 and 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);   // row_bcast:31, rows 2 and 3
+    return x;
+}
+
 // Zero `bytes` of device memory and wait for that alone: on a private
 // non-blocking stream (default priority), so that work already queued on the
 // caller's streams is not waited for.  For handle set-up, never inside a
