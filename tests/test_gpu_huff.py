@@ -243,6 +243,34 @@ def test_reuse_and_batch_of_calls(orc):
             assert int(st.item()) == 0 and np.array_equal(out.cpu().numpy(), values[idx])
 
 
+def test_two_handles_on_two_streams():
+    # two handles decoding at the same time on two streams, each with its own
+    # one-launch hand-off words, eight calls each, not synchronised between
+    rng = np.random.default_rng(12)
+    jobs = []
+    for n in (60000, 45000):
+        idx = H.skewed_stream(rng, 40, n, 1.1)
+        values, lengths = H.table_for(idx, 40, rng)
+        data, n_bits = H.encode(idx, list(lengths))
+        jobs.append((torch.from_numpy(np.frombuffer(data, np.uint8).copy()).to(DEV), n_bits,
+                     torch.from_numpy(values).to(DEV), torch.from_numpy(lengths).to(DEV), n, values[idx]))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    handles = [pkg.HuffDecoder(1 << 20), pkg.HuffDecoder(1 << 20)]
+    outs = [[], []]
+    torch.cuda.synchronize()
+    for _ in range(8):
+        for j in range(2):
+            d, n_bits, v, ln, n, _ = jobs[j]
+            with torch.cuda.stream(streams[j]):
+                outs[j].append(handles[j].decode(d, n_bits, v, ln, n, stream=streams[j].cuda_stream))
+    torch.cuda.synchronize()
+    for j in range(2):
+        for out, st in outs[j]:
+            assert int(st.item()) == 0 and np.array_equal(out.cpu().numpy(), jobs[j][5])
+    for h in handles:
+        h.close()
+
+
 def test_argument_rejection():
     with pkg.HuffDecoder(4096) as h:
         buf = torch.zeros(1024, dtype=torch.uint8, device=DEV)

@@ -353,6 +353,35 @@ def test_runs_on_caller_stream():
     assert np.array_equal(got, ref)
 
 
+def test_two_handles_on_two_streams():
+    """Two handles decoding batches at the same time on two streams (each
+    batch takes tiles from its handle's counters), eight calls each with no
+    synchronisation between them: every output equals a run on its own."""
+    from paper_2609_09020_amd import Decoder
+    inps = [synth.make_inputs(256, 384, 7, (7, 40, 40, 3), batch=8, seed=s, latent_scale=2.0, bias="normal")
+            for s in (41, 42)]
+    decs = [Decoder(256, 384, (7, 40, 40, 3), clamp=False, max_batch=8, variant="mfma_f32") for _ in range(2)]
+    devin = [_to_dev(inp) for inp in inps]
+    want = []
+    for j in range(2):
+        o = decs[j].alloc_out(8, "cuda")
+        decs[j].run(*devin[j], out=o)
+        torch.cuda.synchronize()
+        want.append(o.cpu().numpy())
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[decs[j].alloc_out(8, "cuda") for _ in range(8)] for j in range(2)]
+    torch.cuda.synchronize()
+    for k in range(8):
+        for j in range(2):
+            with torch.cuda.stream(streams[j]):
+                decs[j].run(*devin[j], out=outs[j][k], stream=streams[j].cuda_stream)
+    torch.cuda.synchronize()
+    for j in range(2):
+        for k in range(8):
+            assert np.array_equal(outs[j][k].cpu().numpy(), want[j]), (j, k)
+        decs[j].close()
+
+
 def test_create_does_not_wait_for_other_streams():
     """Creating a decode or an entropy-decoding handle clears its device
     memory on a private stream and waits for that alone: about 50 ms of
