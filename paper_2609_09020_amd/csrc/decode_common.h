@@ -9,6 +9,8 @@
 // grid (edge replication).
 #pragma once
 
+#include <utility>
+
 #include "pic_internal.h"
 
 namespace pic {
@@ -204,6 +206,27 @@ __device__ __forceinline__ float row_sum3(float o0, float o1, float o2)
     return __uint_as_float(e[0]) + __uint_as_float(e[1]);
 }
 
+// Index of texel (r, c) in a level with wk columns.  Image sides are below
+// 2^24 and images below 2^31 pixels (the descriptor's limits), so r and wk
+// fit the unsigned 24-bit multiplier and r * wk + c < 2^31: one full-rate
+// multiply-add and one 64-bit address add, where 64-bit index arithmetic
+// takes a quarter-rate multiply and two adds.
+__device__ __forceinline__ uint32_t texel(int r, int wk, int c)
+{
+    return __umul24((uint32_t)r, (uint32_t)wk) + (uint32_t)c;
+}
+
+// Row of tile t in a grid tiles_x tiles wide, t / tiles_x, as the high half of
+// t m for the host's m = ceil(2^32 / tiles_x) = (2^32 + e) / tiles_x, 0 <= e <
+// tiles_x: t m / 2^32 exceeds t / tiles_x by t e / (tiles_x 2^32), which stays
+// below 1 / tiles_x, so the floor is the quotient, while t tiles_x < 2^32.  The
+// host passes m = 0 where that does not hold for every tile of the launch (and
+// for tiles_x = 1), and the division runs instead.
+__device__ __forceinline__ int tile_row(int t, int tiles_x, uint32_t m)
+{
+    return m ? (int)__umulhi((uint32_t)t, m) : t / tiles_x;
+}
+
 // Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
 // (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
 template <int KMAX, int THT = TH>
@@ -223,7 +246,7 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
                 const int i = i0 + tid;
                 if (i0 + kThreads <= n || i < n) {
                     const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
-                    dst[i] = src[(int64_t)r * wk + c];
+                    dst[i] = src[texel(r, wk, c)];
                 }
             }
         }
@@ -258,7 +281,7 @@ __device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], 
         for (int i0 = 0; i0 < n; i0 += kThreads) {
             const int i = min(i0 + tid, n - 1);
             const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
-            v[idx++] = src[(int64_t)r * wk + c];
+            v[idx++] = src[texel(r, wk, c)];
         }
     }
 }
@@ -293,12 +316,29 @@ struct LaneLevel {
     float clx[TWG];   // horizontal lerp weight, per column group
 };
 
-template <int THT = TH>
-__device__ __forceinline__ void lane_level_init(LaneLevel &lv, int k, int lat_base)
+// Lane group g samples level K0 + KS g (level 0 where that level does not
+// exist: its first-layer weights are zero).  The box offset and pitch are
+// picked from the lane groups' four compile-time values: no loop over the
+// levels below, no multiply.
+template <int THT, int K0, int KS>
+__device__ __forceinline__ void lane_level_init(LaneLevel &lv, int g, int L, int lat_base)
 {
-    lv.inv = pow2_neg(k);
-    lv.loff = lat_base + box_offset<THT>(k);
-    lv.pitch = box_pitch(k);
+    const auto pick = [g](int v0, int v1, int v2, int v3) { return g == 0 ? v0 : g == 1 ? v1 : g == 2 ? v2 : v3; };
+    const int k = K0 + KS * g;
+    const bool ok = k < L;
+    lv.inv = pow2_neg(ok ? k : 0);
+    lv.loff = lat_base + (ok ? pick(box_offset<THT>(K0), box_offset<THT>(K0 + KS), box_offset<THT>(K0 + 2 * KS),
+                                    box_offset<THT>(K0 + 3 * KS))
+                              : 0);
+    lv.pitch = ok ? pick(box_pitch(K0), box_pitch(K0 + KS), box_pitch(K0 + 2 * KS), box_pitch(K0 + 3 * KS)) : box_pitch(0);
+}
+
+// lv[s] for lane group g's level A s + KS g, s < N (N = sizeof...(S)).
+template <int THT, int A, int KS, int... S>
+__device__ __forceinline__ void lane_levels_init(LaneLevel (&lv)[sizeof...(S)], int g, int L, int lat_base,
+                                                 std::integer_sequence<int, S...>)
+{
+    (lane_level_init<THT, A * S, KS>(lv[S], g, L, lat_base), ...);
 }
 
 __device__ __forceinline__ void lane_level_tile(LaneLevel &lv, int ty0, int tx0, int tx1, int col)
@@ -348,6 +388,15 @@ __device__ __forceinline__ void store_out(const DecodeParams &p, int64_t o, floa
         else
             static_cast<uint8_t *>(p.out)[o] = (uint8_t)(int)floorf(__builtin_fmaf(cl, 255.0f, 0.5f));
     }
+}
+
+// m for tile_row: ceil(2^32 / tiles_x) when t tiles_x < 2^32 for every tile
+// index t < tiles and tiles_x > 1, else 0 (tile_row divides).
+inline uint32_t tile_row_recip(int tiles_x, int tiles)
+{
+    if (tiles_x < 2 || (uint64_t)tiles * (uint64_t)tiles_x >= (1ULL << 32))
+        return 0;
+    return (uint32_t)(((1ULL << 32) + (uint64_t)tiles_x - 1) / (uint64_t)tiles_x);
 }
 
 // Grid size for a persistent kernel: as many workgroups as fit at once,

@@ -94,7 +94,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // to spare).
 template <int NB, int NH, int LPG, int RPW>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LPG <= 2 ? 4 : 1)))
-void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
+void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, uint32_t tx_recip)
 {
     constexpr int THT = kWaves * RPW;   // tile rows
     using LY = Layout<NB, NH, LPG, THT>;
@@ -120,8 +120,10 @@ void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
     float boxv[box_regs<4 * LPG, THT>()];
-    if (blk < tiles)
-        load_boxes<4 * LPG, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
+    if (blk < tiles) {
+        const int by = tile_row(blk, tiles_x, tx_recip);
+        load_boxes<4 * LPG, THT>(boxv, p, b, by * THT, (blk - by * tiles_x) * TW, tid);
+    }
 
     // ---- stage this image's parameters into LDS in operand layouts (every
     // load in flight before the first store)
@@ -195,11 +197,7 @@ void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
     // ---- the levels this lane samples: LPG g + j, j < LPG (level 0 where the
     // level does not exist; its weights are zero).
     LaneLevel lv[LPG];
-#pragma unroll
-    for (int j = 0; j < LPG; ++j) {
-        const int k = LPG * g + j;
-        lane_level_init<THT>(lv[j], k < L ? k : 0, LY::LAT);
-    }
+    lane_levels_init<THT, 1, LPG>(lv, g, L, LY::LAT, std::make_integer_sequence<int, LPG>{});
 
     const int H = p.H, W = p.W;
     const int64_t plane = (int64_t)H * W;
@@ -216,7 +214,8 @@ void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int tr = tile_row(t, tiles_x, tx_recip);
+        const int ty0 = tr * THT, tx0 = (t - tr * tiles_x) * TW;
         const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
@@ -371,7 +370,7 @@ hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int ti
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_mfma_bf16<NB, NH, LPG, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
-                       tiles_x, tiles);
+                       tiles_x, tiles, tile_row_recip(tiles_x, tiles));
     return hipGetLastError();
 }
 

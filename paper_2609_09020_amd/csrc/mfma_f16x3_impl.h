@@ -273,7 +273,7 @@ __device__ __forceinline__ float wave_max(float x)
 // rows: 8, or 16 when the launch has tiles to spare).
 template <int NB, int NH, int LS, int KSH, int RPW>
 __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blocks_per_image, int tiles_x,
-                                                         int tiles)
+                                                         int tiles, uint32_t tx_recip)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
     constexpr int THT = kWaves * RPW;   // tile rows
@@ -300,8 +300,10 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     // ---- the first tile's latent loads go out first, so their latency
     // overlaps the parameter gather below
     float boxv[box_regs<4 * LS, THT>()];
-    if (blk < tiles)
-        load_boxes<4 * LS, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
+    if (blk < tiles) {
+        const int by = tile_row(blk, tiles_x, tx_recip);
+        load_boxes<4 * LS, THT>(boxv, p, b, by * THT, (blk - by * tiles_x) * TW, tid);
+    }
 
     // ---- this image's parameters, loaded straight into their operand
     // layouts' order (all loads in flight at once); each layer's largest
@@ -395,11 +397,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
     // ---- the level each lane samples as its value q of the first layer:
     // 4q + g (level 0 where that level does not exist; its weights are zero)
     LaneLevel lv[LS];
-#pragma unroll
-    for (int s = 0; s < LS; ++s) {
-        const int k = 4 * s + g;
-        lane_level_init<THT>(lv[s], k < L ? k : 0, LY::LAT);
-    }
+    lane_levels_init<THT, 4, 1>(lv, g, L, LY::LAT, std::make_integer_sequence<int, LS>{});
 
     const int H = p.H, W = p.W;
     const int64_t plane = (int64_t)H * W;
@@ -418,7 +416,8 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int tr = tile_row(t, tiles_x, tx_recip);
+        const int ty0 = tr * THT, tx0 = (t - tr * tiles_x) * TW;
         const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
@@ -569,7 +568,7 @@ hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int ti
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_mfma_f16x3<NB, NH, LS, KSH, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p,
-                       bpi, tiles_x, tiles);
+                       bpi, tiles_x, tiles, tile_row_recip(tiles_x, tiles));
     return hipGetLastError();
 }
 

@@ -90,7 +90,7 @@ __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row
 // ones measured slower at the same register count, so they are not.
 template <int NB, int NH, int LS, int KSH, int RPW>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(RPW == 4 && NB == 4 && LS <= 2 ? 4 : 1)))
-void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
+void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, uint32_t tx_recip)
 {
     static_assert(KSH <= 4 * NB && KSH > 4 * (NB - 1), "KSH must end in the last block");
     constexpr int THT = kWaves * RPW;   // tile rows
@@ -184,8 +184,10 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
             load_all(std::false_type{});
         // the first tile's latent loads go out behind the parameters: loads
         // complete in order, so the stores below need not wait for them
-        if (blk < tiles)
-            load_boxes<4 * LS, THT>(boxv, p, b, (blk / tiles_x) * THT, (blk % tiles_x) * TW, tid);
+        if (blk < tiles) {
+            const int by = tile_row(blk, tiles_x, tx_recip);
+            load_boxes<4 * LS, THT>(boxv, p, b, by * THT, (blk - by * tiles_x) * TW, tid);
+        }
         // zero what lies outside each layer's shape
         const int r1 = row_neuron(col);
 #pragma unroll
@@ -220,11 +222,7 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
     // whose level 4 s + g does not exist sample level 0 instead: their
     // first-layer weights are zero, so the (finite) value is ignored.
     LaneLevel lv[LS];
-#pragma unroll
-    for (int s = 0; s < LS; ++s) {
-        const int k = 4 * s + g;
-        lane_level_init<THT>(lv[s], k < L ? k : 0, LY::LAT);
-    }
+    lane_levels_init<THT, 4, 1>(lv, g, L, LY::LAT, std::make_integer_sequence<int, LS>{});
 
     const int H = p.H, W = p.W;
     const int64_t plane = (int64_t)H * W;
@@ -245,7 +243,8 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles)
         for (int i = tid; i < p.tile_ctr_len; i += kThreads)
             p.tile_ctr_next[i] = 0;
     for (int t = blk;;) {
-        const int ty0 = (t / tiles_x) * THT, tx0 = (t % tiles_x) * TW;
+        const int tr = tile_row(t, tiles_x, tx_recip);
+        const int ty0 = tr * THT, tx0 = (t - tr * tiles_x) * TW;
         const int ty1 = min(ty0 + THT, H) - 1, tx1 = min(tx0 + TW, W) - 1;
 
         if (t != blk) {       // the first tile was staged with the parameters
@@ -395,7 +394,7 @@ hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int ti
     if (nblocks > 0x7fffffff)
         return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_mfma_f32<NB, NH, LS, KSH, RPW>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, p, bpi,
-                       tiles_x, tiles);
+                       tiles_x, tiles, tile_row_recip(tiles_x, tiles));
     return hipGetLastError();
 }
 
