@@ -108,7 +108,7 @@ enum {
  * sizeof(pic_decode_desc) (the library rejects sizes it does not know). */
 typedef struct pic_decode_desc {
     uint32_t struct_size;
-    int32_t height, width;                  /* H, W in [1, 2^24), H * W < 2^31  */
+    int32_t height, width;                  /* H, W in [1, 2^23), H * W < 2^31  */
     int32_t num_levels;                     /* L in [1, PIC_MAX_LEVELS]          */
     int32_t num_layers;                     /* linear layers in [1, PIC_MAX_LAYERS] */
     int32_t widths[PIC_MAX_LAYERS + 1];     /* widths[0] == L, widths[num_layers] == 3,

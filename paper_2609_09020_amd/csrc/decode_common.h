@@ -46,11 +46,18 @@ __host__ __device__ constexpr int box_offset(int k)
 
 __device__ __forceinline__ float pow2_neg(int k) { return __int_as_float((127 - k) << 23); }
 
-// floor of the clamped source coordinate max((o + 1/2) 2^-k - 1/2, 0).
-__device__ __forceinline__ int src_floor(int o, float inv)
+// floor of the clamped source coordinate max((o + 1/2) 2^-k - 1/2, 0), which is
+// (2 o + 1 - 2^k) / 2^(k+1): the arithmetic shift floors it, exactly.
+__host__ __device__ constexpr int src_floor(int o, int k)
 {
-    const float s = ((float)o + 0.5f) * inv - 0.5f;
-    return s <= 0.0f ? 0 : (int)s;
+    return (2 * o + 1 - (1 << k)) >> (k + 1) > 0 ? (2 * o + 1 - (1 << k)) >> (k + 1) : 0;
+}
+
+// Image b's copy of latent level k: b hk wk texels past image 0's (hk wk <
+// 2^31, so a 32 x 32-bit product)
+__device__ __forceinline__ const float *level_base(const DecodeParams &p, int k, int b)
+{
+    return p.lat[k] + (uint64_t)(uint32_t)b * (uint32_t)(p.hk[k] * p.wk[k]);
 }
 
 // Image b's copy of layer l's parameters (wave-uniform pointers).
@@ -207,7 +214,7 @@ __device__ __forceinline__ float row_sum3(float o0, float o1, float o2)
 }
 
 // Index of texel (r, c) in a level with wk columns.  Image sides are below
-// 2^24 and images below 2^31 pixels (the descriptor's limits), so r and wk
+// 2^23 and images below 2^31 pixels (the descriptor's limits), so r and wk
 // fit the unsigned 24-bit multiplier and r * wk + c < 2^31: one full-rate
 // multiply-add and one 64-bit address add, where 64-bit index arithmetic
 // takes a quarter-rate multiply and two adds.
@@ -235,10 +242,9 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
         if (k < p.L) {
-            const float iv = pow2_neg(k);
             const int hk = p.hk[k], wk = p.wk[k];
-            const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
-            const float *src = p.lat[k] + (int64_t)b * hk * wk;
+            const int ry = src_floor(ty0, k), rx = src_floor(tx0, k);
+            const float *src = level_base(p, k, b);
             float *dst = lat + box_offset<THT>(k);
             const int n = box_floats<THT>(k), pc = box_pitch(k);   // constants once unrolled
 #pragma unroll
@@ -271,11 +277,10 @@ __device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], 
     int idx = 0;
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
-        const float iv = pow2_neg(k);
         // levels past L load level 0 (their slots repeat it; never stored)
         const int hk = p.hk[k], wk = p.wk[k];
-        const int ry = src_floor(ty0, iv), rx = src_floor(tx0, iv);
-        const float *src = p.lat[k] + (int64_t)b * hk * wk;
+        const int ry = src_floor(ty0, k), rx = src_floor(tx0, k);
+        const float *src = level_base(p, k, b);
         const int n = box_floats<THT>(k), pc = box_pitch(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {
@@ -343,8 +348,9 @@ __device__ __forceinline__ void lane_levels_init(LaneLevel (&lv)[sizeof...(S)], 
 
 __device__ __forceinline__ void lane_level_tile(LaneLevel &lv, int ty0, int tx0, int tx1, int col)
 {
-    const int rx = src_floor(tx0, lv.inv);
-    lv.rbase = src_floor(ty0, lv.inv);
+    const int k = 127 - (__float_as_int(lv.inv) >> 23);   // lv.inv = 2^-k
+    const int rx = src_floor(tx0, k);
+    lv.rbase = src_floor(ty0, k);
 #pragma unroll
     for (int cg = 0; cg < TWG; ++cg) {
         const int x = min(tx0 + 16 * cg + col, tx1);

@@ -105,7 +105,9 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
     const int g = lane >> 4, col = lane & 15;
     // images interleave over the grid, so that every image's workgroups are
     // spread over the dispatch order (older workgroups on a CU run ahead)
-    const int b = blockIdx.x % p.batch;
+    int b = 0;
+    if (p.batch > 1)
+        b = blockIdx.x % p.batch;
     const TileSchedule ts = tile_schedule(p, blockIdx.x, blocks_per_image, tiles);
     const int blk = ts.first;
     const int L = p.L;
@@ -228,7 +230,7 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
     const int64_t plane = (int64_t)H * W;
     // Lane group g (< 3) stores channel g; lane group 0 carries the output
     // biases in its partial sums.
-    const int64_t obase = (int64_t)b * 3 * plane + (int64_t)min(g, 2) * plane;
+    const int64_t obase = (int64_t)(uint64_t)(uint32_t)(3 * b + min(g, 2)) * plane;
     const float ob0 = g == 0 ? b3_0 : 0.0f, ob1 = g == 0 ? b3_1 : 0.0f, ob2 = g == 0 ? b3_2 : 0.0f;
     constexpr int KS1 = KSH;   // live registers of a hidden activation
     constexpr int W3NB = 2;   // (larger chunks raise the VGPR count of the wider shapes)
@@ -274,7 +276,7 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
 #pragma unroll
             for (int s = 0; s < LS; ++s)
                 lane_level_row(lv[s], y, roff[s], rly[s]);
-            const int64_t orow = obase + (int64_t)y * W + tx0 + col;
+            const int64_t orow = obase + (uint32_t)(y * W + tx0 + col);   // < H W + 64 <= 2^31 + 63
 
 #pragma unroll
             for (int cg = 0; cg < TWG; ++cg) {

@@ -38,7 +38,7 @@ pic_status validate_desc(const pic_decode_desc *d)
 {
     if (!d || d->struct_size != sizeof(pic_decode_desc))
         return PIC_E_INVALID;
-    if (d->height < 1 || d->width < 1 || d->height >= (1 << 24) || d->width >= (1 << 24) ||
+    if (d->height < 1 || d->width < 1 || d->height >= (1 << 23) || d->width >= (1 << 23) ||
         (int64_t)d->height * d->width >= (1LL << 31))
         return PIC_E_INVALID;
     if (d->num_levels < 1 || d->num_levels > PIC_MAX_LEVELS)

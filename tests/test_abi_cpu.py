@@ -94,7 +94,7 @@ def _gpu_present():
     dict(widths=(4, 129, 3)), dict(widths=(4, 16, 129, 3)), dict(widths=(4, 0, 3)), dict(weight_dtype=2), dict(out_dtype=1),
     dict(flags=2), dict(flags=D.PIC_FLAG_NO_CLAMP, out_dtype=D.PIC_U8), dict(max_batch=0),
     dict(max_batch=70000), dict(variant=9), dict(variant=5), dict(height=65536, width=32768),
-    dict(height=1, width=1 << 24), dict(height=1 << 24, width=1),
+    dict(height=1, width=1 << 23), dict(height=1 << 23, width=1),
     dict(widths=(13,) + (16,) * 2 + (3,)),
 ])
 def test_invalid_descriptors(kw):
@@ -132,9 +132,9 @@ def test_widest_descriptors_pass_validation():
     assert _create_status(widths=(4, 128, 3)) == D.PIC_E_NODEVICE
     assert _create_status(widths=(12,) + (128,) * 7 + (3,)) == D.PIC_E_NODEVICE
     assert _create_status(widths=(12,) + (128,) * 7 + (3,), variant=D.PIC_VARIANT_VALU) == D.PIC_E_NODEVICE
-    # and so are the longest image sides, 2^24 - 1
-    assert _create_status(height=1, width=(1 << 24) - 1) == D.PIC_E_NODEVICE
-    assert _create_status(height=(1 << 24) - 1, width=1) == D.PIC_E_NODEVICE
+    # and so are the longest image sides, 2^23 - 1
+    assert _create_status(height=1, width=(1 << 23) - 1) == D.PIC_E_NODEVICE
+    assert _create_status(height=(1 << 23) - 1, width=1) == D.PIC_E_NODEVICE
 
 
 @pytest.mark.skipif(_gpu_present(), reason="checks the no-device path")
