@@ -234,34 +234,10 @@ __device__ __forceinline__ int tile_row(int t, int tiles_x, uint32_t m)
     return m ? (int)__umulhi((uint32_t)t, m) : t / tiles_x;
 }
 
-// Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
-// (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
-template <int KMAX, int THT = TH>
-__device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, int b, int ty0, int tx0, int tid)
-{
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-        if (k < p.L) {
-            const int hk = p.hk[k], wk = p.wk[k];
-            const int ry = src_floor(ty0, k), rx = src_floor(tx0, k);
-            const float *src = level_base(p, k, b);
-            float *dst = lat + box_offset<THT>(k);
-            const int n = box_floats<THT>(k), pc = box_pitch(k);   // constants once unrolled
-#pragma unroll
-            for (int i0 = 0; i0 < n; i0 += kThreads) {
-                const int i = i0 + tid;
-                if (i0 + kThreads <= n || i < n) {
-                    const int r = min(ry + i / pc, hk - 1), c = min(rx + i % pc, wk - 1);
-                    dst[i] = src[texel(r, wk, c)];
-                }
-            }
-        }
-    }
-}
-
-// The same staging split into a load phase (into registers) and a store
-// phase, so the loads can be in flight while other prologue work waits on
-// memory.  box_regs<KMAX>() registers per thread.
+// Box staging in a load phase (into registers) and a store phase, so that
+// every load is in flight before the first is waited for (and, in the
+// prologue, while the parameter loads are).  box_regs<KMAX>() registers per
+// thread; levels past L load level 0 and are not stored.
 template <int THT>
 __host__ __device__ constexpr int box_regs_from(int k, int kmax)
 {
@@ -307,6 +283,20 @@ __device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_re
             ++idx;
         }
     }
+}
+
+// Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
+// (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
+// Every load is issued before the first store, so a tile waits for one
+// memory round trip, not one per level.  The thread's box indices are
+// derived here, per tile, rather than held in registers from the prologue.
+template <int KMAX, int THT = TH>
+__device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, int b, int ty0, int tx0, int tid)
+{
+    asm volatile("" : "+v"(tid));
+    float v[box_regs<KMAX, THT>()];
+    load_boxes<KMAX, THT>(v, p, b, ty0, tx0, tid);
+    store_boxes<KMAX, THT>(lat, v, p, tid);
 }
 
 // One lane's view of one level for the current tile: where its box starts in

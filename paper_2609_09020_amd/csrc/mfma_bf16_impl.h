@@ -377,8 +377,8 @@ hipError_t launch_rows(const DecodeParams &p, hipStream_t s, int tiles_x, int ti
 }
 
 // 32- or 16-row tiles when every workgroup of the launch averages two or
-// more of them and the taller boxes cost no occupancy (as in the fp32
-// family), else 8-row.
+// more of them and the taller boxes keep 4 wavefronts per SIMD (or the
+// 8-row instance's occupancy, if lower), else 8-row.
 template <int NB, int NH, int LPG>
 hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
 {
@@ -391,9 +391,12 @@ hipError_t launch(const DecodeParams &p, hipStream_t s, int num_cus)
     const int tiles32 = tiles_x * ((p.H + 8 * kWaves - 1) / (8 * kWaves));
     static int occ32 = 0;
     const int bpi32 = blocks_per_image(k_mfma_bf16<NB, NH, LPG, 8>, p, num_cus, tiles32, occ32);
-    if (occ32 >= occ8 && tiles32 >= 2 * bpi32)
+    // (4 wavefronts per SIMD hide the tile loop's latencies: the 32-row
+    // tiles' smaller share of per-tile work outweighs a fifth)
+    const int occ_need = occ8 < 4 ? occ8 : 4;
+    if (occ32 >= occ_need && tiles32 >= 2 * bpi32)
         return launch_rows<NB, NH, LPG, 8>(p, s, tiles_x, tiles32, bpi32);
-    if (occ16 >= occ8 && tiles16 >= 2 * bpi16)
+    if (occ16 >= occ_need && tiles16 >= 2 * bpi16)
         return launch_rows<NB, NH, LPG, 4>(p, s, tiles_x, tiles16, bpi16);
     return launch_rows<NB, NH, LPG, 2>(p, s, tiles_x, tiles8, bpi8);
 }
