@@ -88,11 +88,14 @@ struct LayerParams {
 
 __device__ __forceinline__ LayerParams layer_params(const DecodeParams &p, int l, int b)
 {
-    const int64_t esize = p.weights_bf16 ? 2 : 4;
     LayerParams lp;
-    lp.w = static_cast<const char *>(p.wl[l]) + (int64_t)b * p.wls[l] * esize;
-    lp.b = p.bl[l] + (int64_t)b * p.bls[l];
+    lp.w = p.wl[l];
+    lp.b = p.bl[l];
     lp.bf16 = p.weights_bf16 != 0;
+    if (b != 0) {   // (uniform) image 0, the one-image case, needs no offsets
+        lp.w = static_cast<const char *>(lp.w) + (int64_t)b * p.wls[l] * (p.weights_bf16 ? 2 : 4);
+        lp.b += (int64_t)b * p.bls[l];
+    }
     return lp;
 }
 
@@ -161,13 +164,14 @@ struct TileSchedule {
 __device__ __forceinline__ TileSchedule tile_schedule(const DecodeParams &p, int block, int bpi, int tiles)
 {
     TileSchedule ts;
-    if (p.batch == 1 && bpi % kXcds == 0) {
-        const int x = block % kXcds;
-        const int r0 = (int)((int64_t)tiles * x / kXcds);
-        ts.first = r0 + block / kXcds;
+    if (p.batch == 1 && (unsigned)bpi % kXcds == 0) {
+        // unsigned 32-bit arithmetic (tiles < 2^23, so 8 tiles fits)
+        const unsigned x = (unsigned)block % kXcds, t = (unsigned)tiles;
+        const int r0 = (int)(t * x / kXcds);
+        ts.first = r0 + (int)((unsigned)block / kXcds);
         ts.ctr = p.tile_ctr + x;
-        ts.base = r0 + bpi / kXcds;
-        ts.end = (int)((int64_t)tiles * (x + 1) / kXcds);
+        ts.base = r0 + (int)((unsigned)bpi / kXcds);
+        ts.end = (int)(t * (x + 1) / kXcds);
     } else {
         const int b = block % p.batch;
         ts.first = block / p.batch;
@@ -213,6 +217,13 @@ __device__ __forceinline__ float row_sum3(float o0, float o1, float o2)
     return __uint_as_float(e[0]) + __uint_as_float(e[1]);
 }
 
+// A raw buffer over the n_bytes at p: the hardware's range check returns 0
+// for a load at a byte offset past n_bytes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void *p, unsigned n_bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)n_bytes, 0x00020000);
+}
+
 // Index of texel (r, c) in a level with wk columns.  Image sides are below
 // 2^23 and images below 2^31 pixels (the descriptor's limits), so r and wk
 // fit the unsigned 24-bit multiplier and r * wk + c < 2^31: one full-rate
@@ -250,13 +261,24 @@ template <int KMAX, int THT = TH>
 __device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], const DecodeParams &p, int b, int ty0,
                                            int tx0, int tid)
 {
+    // image b's copies of the levels (one uniform branch: image 0, the
+    // one-image case, skips the offsets)
+    const float *src0[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k)
+        src0[k] = p.lat[k];
+    if (b != 0) {
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k)
+            src0[k] = level_base(p, k, b);
+    }
     int idx = 0;
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
         // levels past L load level 0 (their slots repeat it; never stored)
         const int hk = p.hk[k], wk = p.wk[k];
         const int ry = src_floor(ty0, k), rx = src_floor(tx0, k);
-        const float *src = level_base(p, k, b);
+        const float *src = src0[k];
         const int n = box_floats<THT>(k), pc = box_pitch(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {
@@ -267,9 +289,11 @@ __device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], 
     }
 }
 
+// Every store is unconditional: levels past L (whose loads repeat level 0)
+// go to boxes no lane samples, and the threads past a box's last entry,
+// which loaded that entry, write it again with the value it holds.
 template <int KMAX, int THT = TH>
-__device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_regs<KMAX, THT>())], const DecodeParams &p,
-                                            int tid)
+__device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_regs<KMAX, THT>())], int tid)
 {
     int idx = 0;
 #pragma unroll
@@ -277,10 +301,8 @@ __device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_re
         const int n = box_floats<THT>(k);
 #pragma unroll
         for (int i0 = 0; i0 < n; i0 += kThreads) {
-            const int i = i0 + tid;
-            if (k < p.L && i < n)
-                lat[box_offset<THT>(k) + i] = v[idx];
-            ++idx;
+            const int i = i0 + kThreads <= n ? i0 + tid : min(i0 + tid, n - 1);
+            lat[box_offset<THT>(k) + i] = v[idx++];
         }
     }
 }
@@ -296,7 +318,7 @@ __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, i
     asm volatile("" : "+v"(tid));
     float v[box_regs<KMAX, THT>()];
     load_boxes<KMAX, THT>(v, p, b, ty0, tx0, tid);
-    store_boxes<KMAX, THT>(lat, v, p, tid);
+    store_boxes<KMAX, THT>(lat, v, tid);
 }
 
 // One lane's view of one level for the current tile: where its box starts in

@@ -192,7 +192,7 @@ void k_mfma_bf16(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, u
         store_part(lds + LY::W3, w3);
     }
     if (blk < tiles)
-        store_boxes<4 * LPG, THT>(lds + LY::LAT, boxv, p, tid);
+        store_boxes<4 * LPG, THT>(lds + LY::LAT, boxv, tid);
     __syncthreads();
 
 

@@ -378,7 +378,7 @@ __global__ __launch_bounds__(kThreads) void k_mfma_f16x3(DecodeParams p, int blo
                 lds[LY::W3 + s] = c < 3 && n < NL ? w3raw[k] : 0.0f;
         }
         if (blk < tiles)
-            store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
+            store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, tid);
         __syncthreads();
         // each layer's weight scale and its inverse (wave-uniform)
 #pragma unroll

@@ -136,49 +136,46 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
         constexpr int RW = N / 4;                  // matrix rows per wavefront
         float hrow[NH > 0 ? NH : 1][RW];
         float bv, w3v;
-        // Every load reads an in-range entry (indices clamped into the
-        // arrays) and none sits behind a branch or feeds a select before the
-        // last load is issued: entries outside a layer's shape are zeroed
-        // when stored, after the latent loads have gone out, so no wait is
-        // placed between the loads.  A row's address is uniform (scalar
-        // registers) plus the lane's byte offset, the same for every row.
+        // The parameters are read through raw buffers whose range check
+        // returns 0 past each array's end, so no index is clamped to stay in
+        // bounds: rows past a layer's outputs read 0, and entries of a row
+        // past the layer's inputs (which read the next row) are zeroed when
+        // stored.  No load sits behind a branch or feeds a select before the
+        // last load is issued, so no wait is placed between them.  A hidden
+        // matrix row's offset is the lane's plus a constant per row.
         const int lw = min(wave, NH), l3 = min(wave, 2);    // bias layer / output row of this wavefront
         auto load_all = [&](auto bf16) {
             constexpr bool BF = decltype(bf16)::value;
-            using T = typename std::conditional<BF, uint16_t, float>::type;
-            auto widen = [](T v) {
+            constexpr unsigned ES = BF ? 2 : 4;
+            auto ld = [](__amdgpu_buffer_rsrc_t r, unsigned byte_off) {
                 if constexpr (BF)
-                    return __uint_as_float((uint32_t)v << 16);
+                    return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, byte_off, 0, 0) << 16);
                 else
-                    return v;
-            };
-            auto at = [](const T *row, unsigned byte_off) {
-                return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(row) + byte_off);
+                    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
             };
             // layer 1, A operand: lane (g, i) holds W1[16 ob + rn(i)][4 s + g]
-            const T *w1p = static_cast<const T *>(lp[0].w);
-            const int r1 = row_neuron(col);
+            const auto w1b = raw_buffer(lp[0].w, (unsigned)(N1 * L) * ES);
+            const unsigned w1o = (unsigned)(row_neuron(col) * L + g) * ES;
 #pragma unroll
             for (int ob = 0; ob < NB; ++ob)
 #pragma unroll
                 for (int s = 0; s < LS; ++s)
-                    w1[ob][s] = widen(w1p[min(16 * ob + r1, N1 - 1) * L + min(4 * s + g, L - 1)]);
+                    w1[ob][s] = ld(w1b, w1o + (unsigned)(16 * ob * L + 4 * s) * ES);
             // hidden layer h: wavefront w copies rows w, w + 4, ..., lane c column c
 #pragma unroll
             for (int h = 0; h < NH; ++h) {
                 const int fin = wd[1 + h], fout = wd[2 + h];
-                const T *wp = static_cast<const T *>(lp[1 + h].w);
-                const unsigned cb = (unsigned)min(lane, fin - 1) * sizeof(T);
+                const auto hb = raw_buffer(lp[1 + h].w, (unsigned)(fout * fin) * ES);
+                const unsigned o0 = (unsigned)(wave * fin + lane) * ES, step = (unsigned)(4 * fin) * ES;
 #pragma unroll
                 for (int t = 0; t < RW; ++t)
-                    hrow[h][t] = widen(at(wp + (int64_t)min(wave + 4 * t, fout - 1) * fin, cb));
+                    hrow[h][t] = ld(hb, o0 + t * step);
             }
             // the bias of layer min(w, NH); row min(w, 2) of the output layer
-            // (kernel-argument arrays indexed by the uniform wave number)
-            const float *bsrc = p.bl[lw] + (int64_t)b * p.bls[lw];
-            bv = bsrc[min(lane, p.widths[1 + lw] - 1)];
-            const T *w3p = static_cast<const T *>(lp[NH + 1].w) + l3 * NL;
-            w3v = widen(at(w3p, (unsigned)min(lane, NL - 1) * sizeof(T)));
+            const LayerParams lb = layer_params(p, lw, b);
+            bv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                raw_buffer(lb.b, (unsigned)p.widths[1 + lw] * 4), (unsigned)lane * 4, 0, 0));
+            w3v = ld(raw_buffer(lp[NH + 1].w, (unsigned)(3 * NL) * ES), (unsigned)(l3 * NL + lane) * ES);
         };
         if (lp[0].bf16)
             load_all(std::true_type{});
@@ -205,19 +202,18 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
 #pragma unroll
             for (int h = 0; h < NH; ++h) {
                 const bool cin = lane < wd[1 + h];
-                const int fout = wd[2 + h];
 #pragma unroll
                 for (int t = 0; t < RW; ++t)
-                    wrow[(h * N + 16 * (t >> 2) + (t & 3)) * PITCH] = (cin && wave + 4 * t < fout) ? hrow[h][t] : 0.0f;
+                    wrow[(h * N + 16 * (t >> 2) + (t & 3)) * PITCH] = cin ? hrow[h][t] : 0.0f;
             }
             if (wave <= NH)
-                lds[LY::BIAS + wave * N + sc] = lane < p.widths[1 + lw] ? bv : 0.0f;
+                lds[LY::BIAS + wave * N + sc] = bv;
             if (wave < 3)
                 lds[LY::W3 + wave * N + sc] = lane < NL ? w3v : 0.0f;
         }
     }
     if (blk < tiles)
-        store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, p, tid);
+        store_boxes<4 * LS, THT>(lds + LY::LAT, boxv, tid);
     __syncthreads();
 
     // ---- the level each lane samples for K step s of the first layer.  Lanes
