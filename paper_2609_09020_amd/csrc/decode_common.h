@@ -242,7 +242,10 @@ __device__ __forceinline__ uint32_t texel(int r, int wk, int c)
 // for tiles_x = 1), and the division runs instead.
 __device__ __forceinline__ int tile_row(int t, int tiles_x, uint32_t m)
 {
-    return m ? (int)__umulhi((uint32_t)t, m) : t / tiles_x;
+    if (m)
+        return (int)__umulhi((uint32_t)t, m);
+    asm volatile("" : "+s"(tiles_x));   // (keeps the division's set-up on this path)
+    return t / tiles_x;
 }
 
 // Box staging in a load phase (into registers) and a store phase, so that
@@ -259,24 +262,24 @@ __host__ __device__ constexpr int box_regs() { return box_regs_from<THT>(0, KMAX
 
 template <int KMAX, int THT = TH>
 __device__ __forceinline__ void load_boxes(float (&v)[(box_regs<KMAX, THT>())], const DecodeParams &p, int b, int ty0,
-                                           int tx0, int tid)
+                                           int tx0, int tid, int z = 0)
 {
     // image b's copies of the levels (one uniform branch: image 0, the
     // one-image case, skips the offsets)
     const float *src0[KMAX];
 #pragma unroll
     for (int k = 0; k < KMAX; ++k)
-        src0[k] = p.lat[k];
+        src0[k] = p.lat[k + z];
     if (b != 0) {
 #pragma unroll
         for (int k = 0; k < KMAX; ++k)
-            src0[k] = level_base(p, k, b);
+            src0[k] = level_base(p, k + z, b);
     }
     int idx = 0;
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) {
         // levels past L load level 0 (their slots repeat it; never stored)
-        const int hk = p.hk[k], wk = p.wk[k];
+        const int hk = p.hk[k + z], wk = p.wk[k + z];
         const int ry = src_floor(ty0, k), rx = src_floor(tx0, k);
         const float *src = src0[k];
         const int n = box_floats<THT>(k), pc = box_pitch(k);
@@ -310,14 +313,18 @@ __device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_re
 // Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
 // (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
 // Every load is issued before the first store, so a tile waits for one
-// memory round trip, not one per level.  The thread's box indices are
-// derived here, per tile, rather than held in registers from the prologue.
+// memory round trip, not one per level.  The thread's box indices and the
+// levels' geometry are derived here, per tile.
 template <int KMAX, int THT = TH>
 __device__ __forceinline__ void stage_boxes(float *lat, const DecodeParams &p, int b, int ty0, int tx0, int tid)
 {
-    asm volatile("" : "+v"(tid));
+    // (the levels are indexed with an opaque zero added, so that nothing
+    // derived from their geometry is hoisted into the prologue either, which
+    // one-tile launches would pay for without staging a second tile)
+    int z = 0;
+    asm volatile("" : "+s"(z), "+v"(tid));
     float v[box_regs<KMAX, THT>()];
-    load_boxes<KMAX, THT>(v, p, b, ty0, tx0, tid);
+    load_boxes<KMAX, THT>(v, p, b, ty0, tx0, tid, z);
     store_boxes<KMAX, THT>(lat, v, tid);
 }
 
