@@ -81,6 +81,18 @@ struct Layout {
 // Neuron on row `row` of an output block; the map is its own inverse.
 __device__ __forceinline__ int row_neuron(int row) { return 4 * (row & 3) + (row >> 2); }
 
+// s_setprio with a run-time level in 0 .. 3 (the instruction takes an
+// immediate)
+__device__ __forceinline__ void set_priority(int level)
+{
+    switch (level) {
+    case 3: __builtin_amdgcn_s_setprio(3); break;
+    case 2: __builtin_amdgcn_s_setprio(2); break;
+    case 1: __builtin_amdgcn_s_setprio(1); break;
+    default: __builtin_amdgcn_s_setprio(0); break;
+    }
+}
+
 // NB: 16-neuron blocks of the hidden width; NH: hidden layers; LS: K steps of
 // the first layer (ceil(L / 4)); KSH: K steps of the hidden layers (inputs
 // 4 KSH and up are padding and skipped); RPW: tile rows per wavefront (a tile
@@ -187,13 +199,15 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
             const int by = tile_row(blk, tiles_x, tx_recip);
             load_boxes<4 * LS, THT>(boxv, p, b, by * THT, (blk - by * tiles_x) * TW, tid);
         }
-        // zero what lies outside each layer's shape
-        const int r1 = row_neuron(col);
+        // zero what lies outside each layer's shape.  The first layer's rows
+        // past its outputs read 0; of its inputs only the last K step's can
+        // lie past L (4 (LS - 1) < L), and those read the next row.
+        {
+            const bool in_l = 4 * (LS - 1) + g < L;
 #pragma unroll
-        for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-            for (int s = 0; s < LS; ++s)
-                w1[ob][s] = (16 * ob + r1 < N1 && 4 * s + g < L) ? w1[ob][s] : 0.0f;
+            for (int ob = 0; ob < NB; ++ob)
+                w1[ob][LS - 1] = in_l ? w1[ob][LS - 1] : 0.0f;
+        }
         if (lane < N) {
             // row wave + 4 t goes to swz(wave + 4 t) = 16 (t / 4) + 4 wave + t % 4
             // (wave < 4): a per-lane base plus a constant per row
@@ -285,6 +299,8 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
                 // the previous group (the paper-shaped net 13.3 -> 13.1 us).
                 if constexpr (NB > 1 || RPW > 2)
                     asm volatile("" ::: "memory");
+                if constexpr (RPW == 2 && NB > 1)
+                    set_priority((rr == 0 ? 3 : 1) - cg / 2);
 
                 // layer 1: K = levels, B operand = upsampled pyramid
                 f32x4 d[NB];
