@@ -165,7 +165,7 @@ __device__ __forceinline__ TileSchedule tile_schedule(const DecodeParams &p, int
 {
     TileSchedule ts;
     if (p.batch == 1 && (unsigned)bpi % kXcds == 0) {
-        // unsigned 32-bit arithmetic (tiles < 2^23, so 8 tiles fits)
+        // unsigned 32-bit arithmetic (tiles < 2^23, so 8 tiles < 2^32)
         const unsigned x = (unsigned)block % kXcds, t = (unsigned)tiles;
         const int r0 = (int)(t * x / kXcds);
         ts.first = r0 + (int)((unsigned)block / kXcds);
@@ -251,7 +251,7 @@ __device__ __forceinline__ int tile_row(int t, int tiles_x, uint32_t m)
 // Box staging in a load phase (into registers) and a store phase, so that
 // every load is in flight before the first is waited for (and, in the
 // prologue, while the parameter loads are).  box_regs<KMAX>() registers per
-// thread; levels past L load level 0 and are not stored.
+// thread; levels past L load level 0 (into boxes no lane samples).
 template <int THT>
 __host__ __device__ constexpr int box_regs_from(int k, int kmax)
 {
@@ -310,9 +310,9 @@ __device__ __forceinline__ void store_boxes(float *lat, const float (&v)[(box_re
     }
 }
 
-// Stage the boxes of levels 0 .. min(L, KMAX) - 1 of image b for the tile at
-// (ty0, tx0) into lat (box k at lat + box_offset(k)); all threads take part.
-// Every load is issued before the first store, so a tile waits for one
+// Stage the boxes of levels 0 .. KMAX - 1 of image b for the tile at (ty0,
+// tx0) into lat (box k at lat + box_offset(k); those past L repeat level 0
+// and are not sampled); all threads take part.  Every load is issued before the first store, so a tile waits for one
 // memory round trip, not one per level.  The thread's box indices and the
 // levels' geometry are derived here, per tile.
 template <int KMAX, int THT = TH>

@@ -274,6 +274,9 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
         // A wavefront's priority is raised for the first row of each tile and
         // dropped after it, so that the wavefronts of a SIMD progress together
         // instead of oldest first, and none is left to run alone at the end.
+        // Nets of two or more blocks on 8-row tiles (one tile per workgroup
+        // in small launches) step it down per 16-pixel group instead: 3, 3,
+        // 2, 2 over the first row, 1, 1, 0, 0 over the second.
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll 1
         for (int rr = 0; rr < RPW; ++rr) {
