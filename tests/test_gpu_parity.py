@@ -245,6 +245,27 @@ def test_fuzz_raw(case, variant):
     _run_case(case, variant)
 
 
+# The longest image sides the descriptor accepts, 2^23 - 1 (pixel centres
+# and source coordinates exact in fp32, a texel's index in one 24-bit
+# multiply), one pixel across: a single row of 2^17 tiles, where tiles x tiles
+# across >= 2^32 so the tile row comes from the division rather than the
+# multiply-high, and a single column of 2^20 tiles.
+_LONG_REF = {}
+
+
+@pytest.mark.parametrize("variant", F32_VARIANTS)
+@pytest.mark.parametrize("hw", [(1, (1 << 23) - 1), ((1 << 23) - 1, 1)], ids=["row", "column"])
+def test_longest_sides(hw, variant):
+    H, W = hw
+    widths = (4, 16, 16, 3)
+    inp = synth.make_inputs(H, W, widths[0], widths, batch=1, seed=41, latent="normal", latent_scale=1.5,
+                            bias="normal")
+    got, _ = gpu_decode(inp, variant=variant, clamp=False)
+    if hw not in _LONG_REF:
+        _LONG_REF[hw] = oracle.decode_inputs(inp, out="raw")
+    _check_float(got, _LONG_REF[hw], True, f"sides {H}x{W} {variant}")
+
+
 @pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(12, 77), ids=str)
 def test_reference_family_matches_binary32_model(case):
     r = _run_case(case, "valu")
