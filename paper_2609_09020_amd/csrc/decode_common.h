@@ -341,20 +341,26 @@ struct LaneLevel {
 };
 
 // Lane group g samples level K0 + KS g (level 0 where that level does not
-// exist: its first-layer weights are zero).  The box offset and pitch are
-// picked from the lane groups' four compile-time values: no loop over the
-// levels below, no multiply.
+// exist: its first-layer weights are zero).  The four lane groups' box
+// offsets (16 bits each) and pitches (8 bits each) are packed into
+// compile-time constants and picked by shifts: no loop over the levels
+// below, no multiply, no branch.
 template <int THT, int K0, int KS>
 __device__ __forceinline__ void lane_level_init(LaneLevel &lv, int g, int L, int lat_base)
 {
-    const auto pick = [g](int v0, int v1, int v2, int v3) { return g == 0 ? v0 : g == 1 ? v1 : g == 2 ? v2 : v3; };
+    constexpr int K3 = K0 + 3 * KS;
+    static_assert(box_offset<THT>(K3) < 65536 && box_pitch(0) < 256, "packed box geometry");
+    constexpr uint32_t off01 = (uint32_t)box_offset<THT>(K0) | (uint32_t)box_offset<THT>(K0 + KS) << 16;
+    constexpr uint32_t off23 = (uint32_t)box_offset<THT>(K0 + 2 * KS) | (uint32_t)box_offset<THT>(K3) << 16;
+    constexpr uint32_t pitches = (uint32_t)box_pitch(K0) | (uint32_t)box_pitch(K0 + KS) << 8 |
+                                 (uint32_t)box_pitch(K0 + 2 * KS) << 16 | (uint32_t)box_pitch(K3) << 24;
     const int k = K0 + KS * g;
     const bool ok = k < L;
+    const int off = (int)(((g < 2 ? off01 : off23) >> (16 * (g & 1))) & 0xffff);
+    const int pitch = (int)((pitches >> (8 * g)) & 0xff);
     lv.inv = pow2_neg(ok ? k : 0);
-    lv.loff = lat_base + (ok ? pick(box_offset<THT>(K0), box_offset<THT>(K0 + KS), box_offset<THT>(K0 + 2 * KS),
-                                    box_offset<THT>(K0 + 3 * KS))
-                              : 0);
-    lv.pitch = ok ? pick(box_pitch(K0), box_pitch(K0 + KS), box_pitch(K0 + 2 * KS), box_pitch(K0 + 3 * KS)) : box_pitch(0);
+    lv.loff = lat_base + (ok ? off : 0);
+    lv.pitch = ok ? pitch : box_pitch(0);
 }
 
 // lv[s] for lane group g's level A s + KS g, s < N (N = sizeof...(S)).
