@@ -132,9 +132,9 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
     float w1[NB][LS];
 
     // ---- parameters.  Every load is issued before the first is waited for:
-    // the first layer's operands straight into registers, the hidden
-    // matrices' rows, biases and output weights into registers, then the
-    // first tile's latent boxes; after that everything is stored to LDS.
+    // the first tile's latent boxes, then the first layer's operands
+    // straight into registers and the hidden matrices' rows, biases and
+    // output weights into registers; after that everything is stored to LDS.
     {
         LayerParams lp[NH + 2];
         int wd[NH + 3];
@@ -189,16 +189,18 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
                 raw_buffer(lb.b, (unsigned)p.widths[1 + lw] * 4), (unsigned)lane * 4, 0, 0));
             w3v = ld(raw_buffer(lp[NH + 1].w, (unsigned)(3 * NL) * ES), (unsigned)(l3 * NL + lane) * ES);
         };
-        if (lp[0].bf16)
-            load_all(std::true_type{});
-        else
-            load_all(std::false_type{});
-        // the first tile's latent loads go out behind the parameters: loads
-        // complete in order, so the stores below need not wait for them
+        // the first tile's latent loads go out first: every workgroup reads
+        // texels of its own, while the parameters are shared and sit in the
+        // L2 (the parameter stores below then wait for the boxes as well,
+        // which measured cheaper than starting the boxes later)
         if (blk < tiles) {
             const int by = tile_row(blk, tiles_x, tx_recip);
             load_boxes<4 * LS, THT>(boxv, p, b, by * THT, (blk - by * tiles_x) * TW, tid);
         }
+        if (lp[0].bf16)
+            load_all(std::true_type{});
+        else
+            load_all(std::false_type{});
         // zero what lies outside each layer's shape.  The first layer's rows
         // past its outputs read 0; of its inputs only the last K step's can
         // lie past L (4 (LS - 1) < L), and those read the next row.
