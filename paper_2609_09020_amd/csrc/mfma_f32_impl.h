@@ -298,130 +298,223 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
             // pass: their matrix chains interleave and share every weight
             // read.  (The second group of a pair may lie right of the image:
             // its taps read clamped box entries and its store is skipped.)
-            constexpr int G = (RPW == 2 && NB > 1) ? 2 : 1;
+            // The other instances keep one group per pass: the paired code,
+            // instantiated with one group, compiled to more VGPRs.
+            constexpr bool PAIRS = RPW == 2 && NB > 1;
+            if constexpr (PAIRS) {
+                constexpr int G = 2;
 #pragma unroll
-            for (int cg = 0; cg < TWG; cg += G) {
-                if (tx0 + 16 * cg > tx1)
-                    break;   // wave-uniform: the column group lies right of the image
-                // Re-read the LDS operands per pass rather than letting the
-                // compiler keep loop-invariant ones in VGPRs (occupancy).
-                // One-block nets on 8-row tiles (small launches) leave it to
-                // the compiler, which then starts a group's LDS reads during
-                // the previous group (the paper-shaped net 13.3 -> 13.1 us).
-                if constexpr (NB > 1 || RPW > 2)
+                for (int cg = 0; cg < TWG; cg += G) {
+                    if (tx0 + 16 * cg > tx1)
+                        break;   // wave-uniform: the column group lies right of the image
+                    // Re-read the LDS operands per pass rather than letting the
+                    // compiler keep loop-invariant ones in VGPRs (occupancy).
                     asm volatile("" ::: "memory");
-                if constexpr (RPW == 2 && NB > 1)
                     set_priority((rr == 0 ? 3 : 1) - cg / 2);
 
-                // layer 1: K = levels, B operand = upsampled pyramid
-                f32x4 d[G][NB];
-#pragma unroll
-                for (int ob = 0; ob < NB; ++ob) {
-                    const f32x4 bias = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + 16 * ob + 4 * g]);
-#pragma unroll
-                    for (int gi = 0; gi < G; ++gi)
-                        d[gi][ob] = bias;
-                }
-#pragma unroll
-                for (int s = 0; s < LS; ++s) {
-                    float u[G];
-#pragma unroll
-                    for (int gi = 0; gi < G; ++gi)
-                        u[gi] = lane_level_sample(lds, lv[s], roff[s], rly[s], cg + gi);
-#pragma unroll
-                    for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-                        for (int gi = 0; gi < G; ++gi)
-                            d[gi][ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[ob][s], u[gi], d[gi][ob], 0, 0, 0);
-                }
-#pragma unroll
-                for (int gi = 0; gi < G; ++gi)
-#pragma unroll
-                    for (int ks = 0; ks < KS1; ++ks)
-                        d[gi][ks >> 2][ks & 3] = relu(d[gi][ks >> 2][ks & 3]);
-
-                // hidden layers
-#pragma unroll
-                for (int h = 0; h < NH; ++h) {
-                    f32x4 e[G][NB];
+                    // layer 1: K = levels, B operand = upsampled pyramid
+                    f32x4 d[G][NB];
 #pragma unroll
                     for (int ob = 0; ob < NB; ++ob) {
-                        const f32x4 bias =
-                            *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + (1 + h) * N + 16 * ob + 4 * g]);
+                        const f32x4 bias = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + 16 * ob + 4 * g]);
 #pragma unroll
                         for (int gi = 0; gi < G; ++gi)
-                            e[gi][ob] = bias;
+                            d[gi][ob] = bias;
                     }
-                    // A operands of K steps 4q .. 4q+3 come from LDS, one 16-byte
-                    // read per output block; step 4q + j pairs with register j
-                    // of input block q.
 #pragma unroll
-                    for (int q = 0; q < LY::KSH4; ++q) {
-                        f32x4 wq[NB];
+                    for (int s = 0; s < LS; ++s) {
+                        float u[G];
+#pragma unroll
+                        for (int gi = 0; gi < G; ++gi)
+                            u[gi] = lane_level_sample(lds, lv[s], roff[s], rly[s], cg + gi);
 #pragma unroll
                         for (int ob = 0; ob < NB; ++ob)
-                            wq[ob] = *reinterpret_cast<const f32x4 *>(
-                                &lds[LY::WH + (h * N + 16 * ob + col) * PITCH + 16 * q + 4 * g]);
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (4 * q + j < KSH) {
-#pragma unroll
-                                for (int ob = 0; ob < NB; ++ob)
-#pragma unroll
-                                    for (int gi = 0; gi < G; ++gi)
-                                        e[gi][ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wq[ob][j], d[gi][q][j],
-                                                                                         e[gi][ob], 0, 0, 0);
-                            }
-                        }
+                            for (int gi = 0; gi < G; ++gi)
+                                d[gi][ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[ob][s], u[gi], d[gi][ob], 0, 0, 0);
                     }
 #pragma unroll
                     for (int gi = 0; gi < G; ++gi)
 #pragma unroll
                         for (int ks = 0; ks < KS1; ++ks)
-                            d[gi][ks >> 2][ks & 3] = relu(e[gi][ks >> 2][ks & 3]);
-                }
+                            d[gi][ks >> 2][ks & 3] = relu(d[gi][ks >> 2][ks & 3]);
 
-                // output layer on the vector ALU: partial sums over this lane's
-                // live hidden values, then a sum over the four lane groups
-                // (weights of W3NB blocks are read at a time, all before their
-                // first use, so one LDS round trip covers each chunk)
-                float o[G][3];
+                    // hidden layers
 #pragma unroll
-                for (int gi = 0; gi < G; ++gi) {
-                    o[gi][0] = ob0;
-                    o[gi][1] = ob1;
-                    o[gi][2] = ob2;
-                }
+                    for (int h = 0; h < NH; ++h) {
+                        f32x4 e[G][NB];
 #pragma unroll
-                for (int nb0 = 0; nb0 < NB; nb0 += W3NB) {
-                    f32x4 w3[W3NB][3];
+                        for (int ob = 0; ob < NB; ++ob) {
+                            const f32x4 bias =
+                                *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + (1 + h) * N + 16 * ob + 4 * g]);
 #pragma unroll
-                    for (int j = 0; j < W3NB; ++j)
-                        if (nb0 + j < NB)
+                            for (int gi = 0; gi < G; ++gi)
+                                e[gi][ob] = bias;
+                        }
+                        // A operands of K steps 4q .. 4q+3 come from LDS, one 16-byte
+                        // read per output block; step 4q + j pairs with register j
+                        // of input block q.
 #pragma unroll
-                            for (int c = 0; c < 3; ++c)
-                                w3[j][c] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + c * N + 16 * (nb0 + j) + 4 * g]);
+                        for (int q = 0; q < LY::KSH4; ++q) {
+                            f32x4 wq[NB];
 #pragma unroll
-                    for (int j = 0; j < W3NB; ++j) {
+                            for (int ob = 0; ob < NB; ++ob)
+                                wq[ob] = *reinterpret_cast<const f32x4 *>(
+                                    &lds[LY::WH + (h * N + 16 * ob + col) * PITCH + 16 * q + 4 * g]);
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            if (nb0 + j < NB && 4 * (nb0 + j) + r < KS1) {
+                            for (int j = 0; j < 4; ++j) {
+                                if (4 * q + j < KSH) {
 #pragma unroll
-                                for (int gi = 0; gi < G; ++gi) {
-                                    const float hv = d[gi][nb0 + j][r];
-                                    o[gi][0] = __builtin_fmaf(w3[j][0][r], hv, o[gi][0]);
-                                    o[gi][1] = __builtin_fmaf(w3[j][1][r], hv, o[gi][1]);
-                                    o[gi][2] = __builtin_fmaf(w3[j][2][r], hv, o[gi][2]);
+                                    for (int ob = 0; ob < NB; ++ob)
+#pragma unroll
+                                        for (int gi = 0; gi < G; ++gi)
+                                            e[gi][ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wq[ob][j], d[gi][q][j],
+                                                                                             e[gi][ob], 0, 0, 0);
+                                }
+                            }
+                        }
+#pragma unroll
+                        for (int gi = 0; gi < G; ++gi)
+#pragma unroll
+                            for (int ks = 0; ks < KS1; ++ks)
+                                d[gi][ks >> 2][ks & 3] = relu(e[gi][ks >> 2][ks & 3]);
+                    }
+
+                    // output layer on the vector ALU: partial sums over this lane's
+                    // live hidden values, then a sum over the four lane groups
+                    // (weights of W3NB blocks are read at a time, all before their
+                    // first use, so one LDS round trip covers each chunk)
+                    float o[G][3];
+#pragma unroll
+                    for (int gi = 0; gi < G; ++gi) {
+                        o[gi][0] = ob0;
+                        o[gi][1] = ob1;
+                        o[gi][2] = ob2;
+                    }
+#pragma unroll
+                    for (int nb0 = 0; nb0 < NB; nb0 += W3NB) {
+                        f32x4 w3[W3NB][3];
+#pragma unroll
+                        for (int j = 0; j < W3NB; ++j)
+                            if (nb0 + j < NB)
+#pragma unroll
+                                for (int c = 0; c < 3; ++c)
+                                    w3[j][c] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + c * N + 16 * (nb0 + j) + 4 * g]);
+#pragma unroll
+                        for (int j = 0; j < W3NB; ++j) {
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                if (nb0 + j < NB && 4 * (nb0 + j) + r < KS1) {
+#pragma unroll
+                                    for (int gi = 0; gi < G; ++gi) {
+                                        const float hv = d[gi][nb0 + j][r];
+                                        o[gi][0] = __builtin_fmaf(w3[j][0][r], hv, o[gi][0]);
+                                        o[gi][1] = __builtin_fmaf(w3[j][1][r], hv, o[gi][1]);
+                                        o[gi][2] = __builtin_fmaf(w3[j][2][r], hv, o[gi][2]);
+                                    }
                                 }
                             }
                         }
                     }
-                }
 #pragma unroll
-                for (int gi = 0; gi < G; ++gi) {
-                    const float v = row_sum3(o[gi][0], o[gi][1], o[gi][2]);
-                    if (g < 3 && tx0 + 16 * (cg + gi) + col <= tx1)
-                        store_out(p, orow + 16 * (cg + gi), v);
+                    for (int gi = 0; gi < G; ++gi) {
+                        const float v = row_sum3(o[gi][0], o[gi][1], o[gi][2]);
+                        if (g < 3 && tx0 + 16 * (cg + gi) + col <= tx1)
+                            store_out(p, orow + 16 * (cg + gi), v);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int cg = 0; cg < TWG; ++cg) {
+                    if (tx0 + 16 * cg > tx1)
+                        break;   // wave-uniform: the column group lies right of the image
+                    // Re-read the LDS operands per group rather than letting the
+                    // compiler keep loop-invariant ones in VGPRs (occupancy).
+                    // One-block nets on 8-row tiles (small launches) leave it to
+                    // the compiler, which then starts a group's LDS reads during
+                    // the previous group (the paper-shaped net 13.3 -> 13.1 us).
+                    if constexpr (NB > 1 || RPW > 2)
+                        asm volatile("" ::: "memory");
+                    if constexpr (RPW == 2 && NB > 1)
+                        set_priority((rr == 0 ? 3 : 1) - cg / 2);
+
+                    // layer 1: K = levels, B operand = upsampled pyramid
+                    f32x4 d[NB];
+#pragma unroll
+                    for (int ob = 0; ob < NB; ++ob)
+                        d[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + 16 * ob + 4 * g]);
+#pragma unroll
+                    for (int s = 0; s < LS; ++s) {
+                        const float u = lane_level_sample(lds, lv[s], roff[s], rly[s], cg);
+#pragma unroll
+                        for (int ob = 0; ob < NB; ++ob)
+                            d[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[ob][s], u, d[ob], 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks)
+                        d[ks >> 2][ks & 3] = relu(d[ks >> 2][ks & 3]);
+
+                    // hidden layers
+#pragma unroll
+                    for (int h = 0; h < NH; ++h) {
+                        f32x4 e[NB];
+#pragma unroll
+                        for (int ob = 0; ob < NB; ++ob)
+                            e[ob] = *reinterpret_cast<const f32x4 *>(&lds[LY::BIAS + (1 + h) * N + 16 * ob + 4 * g]);
+                        // A operands of K steps 4q .. 4q+3 come from LDS, one 16-byte
+                        // read per output block; step 4q + j pairs with register j
+                        // of input block q.
+#pragma unroll
+                        for (int q = 0; q < LY::KSH4; ++q) {
+                            f32x4 wq[NB];
+#pragma unroll
+                            for (int ob = 0; ob < NB; ++ob)
+                                wq[ob] = *reinterpret_cast<const f32x4 *>(
+                                    &lds[LY::WH + (h * N + 16 * ob + col) * PITCH + 16 * q + 4 * g]);
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                if (4 * q + j < KSH) {
+#pragma unroll
+                                    for (int ob = 0; ob < NB; ++ob)
+                                        e[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(wq[ob][j], d[q][j], e[ob], 0, 0, 0);
+                                }
+                            }
+                        }
+#pragma unroll
+                        for (int ks = 0; ks < KS1; ++ks)
+                            d[ks >> 2][ks & 3] = relu(e[ks >> 2][ks & 3]);
+                    }
+
+                    // output layer on the vector ALU: partial sums over this lane's
+                    // live hidden values, then a sum over the four lane groups
+                    // (weights of W3NB blocks are read at a time, all before their
+                    // first use, so one LDS round trip covers each chunk)
+                    float o0 = ob0, o1 = ob1, o2 = ob2;
+#pragma unroll
+                    for (int nb0 = 0; nb0 < NB; nb0 += W3NB) {
+                        f32x4 w3[W3NB][3];
+#pragma unroll
+                        for (int j = 0; j < W3NB; ++j)
+                            if (nb0 + j < NB)
+#pragma unroll
+                                for (int c = 0; c < 3; ++c)
+                                    w3[j][c] = *reinterpret_cast<const f32x4 *>(&lds[LY::W3 + c * N + 16 * (nb0 + j) + 4 * g]);
+#pragma unroll
+                        for (int j = 0; j < W3NB; ++j) {
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                if (nb0 + j < NB && 4 * (nb0 + j) + r < KS1) {
+                                    const float hv = d[nb0 + j][r];
+                                    o0 = __builtin_fmaf(w3[j][0][r], hv, o0);
+                                    o1 = __builtin_fmaf(w3[j][1][r], hv, o1);
+                                    o2 = __builtin_fmaf(w3[j][2][r], hv, o2);
+                                }
+                            }
+                        }
+                    }
+                    const float v = row_sum3(o0, o1, o2);
+                    if (g < 3 && tx0 + 16 * cg + col <= tx1)
+                        store_out(p, orow + 16 * cg, v);
                 }
             }
             __builtin_amdgcn_s_setprio(0);
