@@ -293,14 +293,14 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
                 lane_level_row(lv[s], y, roff[s], rly[s]);
             const int64_t orow = obase + (uint32_t)(y * W + tx0 + col);   // < H W + 64 <= 2^31 + 63
 
-            // Nets of two or more blocks on 8-row tiles (one-tile launches,
-            // three wavefronts per SIMD) evaluate two 16-pixel groups per
-            // pass: their matrix chains interleave and share every weight
-            // read.  (The second group of a pair may lie right of the image:
-            // its taps read clamped box entries and its store is skipped.)
-            // The other instances keep one group per pass: the paired code,
-            // instantiated with one group, compiled to more VGPRs.
-            constexpr bool PAIRS = RPW == 2 && NB > 1;
+            // 8-row tiles (small launches, mostly one tile per workgroup)
+            // evaluate two 16-pixel groups per pass: their matrix chains
+            // interleave and share every weight read.  (The second group of a
+            // pair may lie right of the image: its taps read clamped box
+            // entries and its store is skipped.)  16-row tiles keep one group
+            // per pass, for occupancy; the paired code instantiated with one
+            // group compiled to more VGPRs, so they keep their own loop.
+            constexpr bool PAIRS = RPW == 2;
             if constexpr (PAIRS) {
                 constexpr int G = 2;
 #pragma unroll
