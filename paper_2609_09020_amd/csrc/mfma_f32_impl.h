@@ -276,9 +276,9 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
         // A wavefront's priority is raised for the first row of each tile and
         // dropped after it, so that the wavefronts of a SIMD progress together
         // instead of oldest first, and none is left to run alone at the end.
-        // Nets of two or more blocks on 8-row tiles (one tile per workgroup
-        // in small launches) step it down per 16-pixel group instead: 3, 3,
-        // 2, 2 over the first row, 1, 1, 0, 0 over the second.
+        // 8-row tiles (one tile per workgroup in small launches) step it
+        // down per pair of 16-pixel groups instead: 3, 2 over the first
+        // row, 1, 0 over the second.
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll 1
         for (int rr = 0; rr < RPW; ++rr) {
@@ -430,13 +430,7 @@ void k_mfma_f32(DecodeParams p, int blocks_per_image, int tiles_x, int tiles, ui
                         break;   // wave-uniform: the column group lies right of the image
                     // Re-read the LDS operands per group rather than letting the
                     // compiler keep loop-invariant ones in VGPRs (occupancy).
-                    // One-block nets on 8-row tiles (small launches) leave it to
-                    // the compiler, which then starts a group's LDS reads during
-                    // the previous group (the paper-shaped net 13.3 -> 13.1 us).
-                    if constexpr (NB > 1 || RPW > 2)
-                        asm volatile("" ::: "memory");
-                    if constexpr (RPW == 2 && NB > 1)
-                        set_priority((rr == 0 ? 3 : 1) - cg / 2);
+                    asm volatile("" ::: "memory");
 
                     // layer 1: K = levels, B operand = upsampled pyramid
                     f32x4 d[NB];
