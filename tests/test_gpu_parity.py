@@ -266,6 +266,23 @@ def test_longest_sides(hw, variant):
     _check_float(got, _LONG_REF[hw], True, f"sides {H}x{W} {variant}")
 
 
+@pytest.mark.parametrize("hw", [(1, (1 << 23) - 1), ((1 << 23) - 1, 1)], ids=["row", "column"])
+def test_longest_sides_bf16(hw):
+    """The bf16-weight matrix family at the longest sides the boundary takes
+    (its tile rows then come from the division, not the multiply-high), the
+    whole output against the fp64 oracle on the same bf16 weights."""
+    H, W = hw
+    widths = (4, 16, 16, 3)
+    inp = synth.make_inputs(H, W, widths[0], widths, batch=1, seed=43, latent="normal", latent_scale=1.5,
+                            bias="normal", weight_dtype="bf16")
+    got, info = gpu_decode(inp, variant="mfma_bf16", clamp=False)
+    assert info["variant"] == "mfma_bf16"
+    ref = oracle.decode_inputs(inp, out="raw")
+    err = np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref)))
+    print(f"PARITY bf16 sides {H}x{W}: max err {err:.3e}", flush=True)
+    assert err <= BF16_TOL
+
+
 @pytest.mark.parametrize("case", EDGE_CASES + _fuzz_cases(12, 77), ids=str)
 def test_reference_family_matches_binary32_model(case):
     r = _run_case(case, "valu")
